@@ -1,0 +1,10 @@
+"""fp64 CPU oracle for MoA attention (test infrastructure only; never on the product path)."""
+from .moa_oracle import (CacheModel, attention_ref, attention_rows_ref, cache_contents_ref,
+                         cache_ref, decode_ref, masked_softmax_rows, plan_ref,
+                         probabilities_ref, visible, visible_mask, visible_set, window_ref)
+
+__all__ = [
+    "CacheModel", "attention_ref", "attention_rows_ref", "cache_contents_ref", "cache_ref",
+    "decode_ref", "masked_softmax_rows", "plan_ref", "probabilities_ref", "visible",
+    "visible_mask", "visible_set", "window_ref",
+]
