@@ -1,0 +1,171 @@
+/*
+ * moa.h - C ABI of the MI355X (gfx950) Mixture-of-Attention-Spans library.
+ *
+ * Mixture of Attention Spans (MoA) gives every attention head (every KV head
+ * under grouped-query attention) its own sliding-window length, set by an
+ * elastic rule over the input length N, plus a few always-visible initial
+ * "sink" tokens.  This library computes that attention on one GPU:
+ *
+ *   moa_plan       per-head window / cache-capacity / cache-offset tables
+ *                  from the rule parameters (paper Sec. 3.2, Eq. 2; span
+ *                  clipping in Appendix "Main Setup").
+ *   moa_prefill    banded-plus-sink causal attention over a whole prompt
+ *                  (paper Sec. 2.1, Eq. 1 with the Sec. 3.2 mask).
+ *   moa_kv_append  writes new tokens into per-head static caches that keep
+ *                  the sinks and the latest window tokens, replacing the
+ *                  oldest non-sink entry in place (paper Appendix
+ *                  "Efficiency Experiment Setup", "Memory and Throughput
+ *                  Breakdown": the cache length equals the span and old
+ *                  entries beyond it are replaced by the latest).
+ *   moa_decode     one query token per sequence against the per-head caches
+ *                  of different lengths (paper Appendix "Efficiency
+ *                  Experiment Setup": decode over KV caches whose length
+ *                  differs across heads).
+ *
+ * Definitions used throughout (s = num_sink, w_g = window of KV head g):
+ *   window    w_g = min(max(floor(alpha_g + beta_g * N), 1), N), evaluated
+ *             in IEEE double without fused multiply-add.
+ *   visible   query position i sees key position j iff j <= i and
+ *             (j < s or i - j < w_g).  The band includes the query itself.
+ *   capacity  C_g = s + w_g cache slots for KV head g.
+ *   slot      position p is stored in slot p if p < s, otherwise in slot
+ *             s + ((p - s) mod w_g); a later position that maps to the same
+ *             slot replaces the earlier one (the earlier one is always the
+ *             oldest non-sink entry).
+ *   scale     scores are scale * (q . k); scale = 1/sqrt(head_dim) when the
+ *             descriptor's softmax_scale is 0.
+ *
+ * Layouts (all row-major, contiguous, element type = the plan's dtype):
+ *   prefill q, o         [batch, n_tokens, num_q_heads,  head_dim]
+ *   prefill k, v, k_new  [batch, n_tokens, num_kv_heads, head_dim]
+ *   decode q, o          [batch, num_q_heads, head_dim]
+ *   k_cache, v_cache     [batch, R, head_dim] with R = offset[num_kv_heads];
+ *                        KV head g owns rows [offset[g], offset[g] + C_g).
+ *   pos_cache            int32 [batch, R]: position held by each slot, -1 if
+ *                        empty.  The caller fills it with -1 before the
+ *                        first append.
+ *   Query head h uses KV head h / (num_q_heads / num_kv_heads).
+ *
+ * Ownership: the caller owns every device buffer (inputs, outputs, caches,
+ * pos_cache, decode workspace).  A plan owns only host memory; it holds no
+ * device memory and may be shared by threads for reading.  moa_prefill,
+ * moa_kv_append and moa_decode allocate nothing.
+ *
+ * Streams: every GPU call only enqueues kernels on `hip_stream` (a
+ * hipStream_t; NULL = the null stream) and returns without synchronizing.
+ * Device pointers must belong to the current HIP device.
+ *
+ * Errors: arguments are validated on the host before anything is launched; a
+ * failed validation returns MOA_ERR_INVALID_ARG / MOA_ERR_UNSUPPORTED /
+ * MOA_ERR_WORKSPACE and launches nothing.  A failed launch returns
+ * MOA_ERR_HIP.  moa_last_error() returns a thread-local message for the last
+ * non-OK status of the calling thread.  Faults inside kernels surface at the
+ * caller's next synchronization, as for any HIP kernel.
+ */
+#ifndef MOA_H_
+#define MOA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  MOA_OK = 0,
+  MOA_ERR_INVALID_ARG = 1,   /* null pointer, bad size, protocol violation */
+  MOA_ERR_UNSUPPORTED = 2,   /* valid but not implemented (head_dim, group size, ...) */
+  MOA_ERR_WORKSPACE = 3,     /* decode workspace missing or too small */
+  MOA_ERR_HIP = 4            /* a HIP launch or runtime call failed */
+} moa_status_t;
+
+typedef enum {
+  MOA_F32 = 0,               /* fp32 in, fp32 accumulate, fp32 out */
+  MOA_BF16 = 1               /* bf16 in, fp32 accumulate, bf16 out (round to nearest even) */
+} moa_dtype_t;
+
+/* Largest supported head counts (the per-head tables travel as kernel arguments). */
+#define MOA_MAX_KV_HEADS 64
+#define MOA_MAX_Q_HEADS 512
+
+/* Attention-layer descriptor.  Supported: head_dim in {64, 128};
+ * num_q_heads % num_kv_heads == 0 with group size in {1, 2, 4, 8};
+ * 0 <= num_sink; 1 <= n < 2^30 ("n" is the input length N at which the
+ * elastic rule is evaluated; windows stay fixed afterwards, during decode). */
+typedef struct {
+  int32_t num_q_heads;
+  int32_t num_kv_heads;
+  int32_t head_dim;
+  int32_t num_sink;
+  int64_t n;
+  int32_t dtype;             /* moa_dtype_t */
+  float softmax_scale;       /* 0 => 1/sqrt(head_dim) */
+} moa_desc_t;
+
+typedef struct moa_plan_s moa_plan_t;
+
+/* Builds the per-KV-head tables for one layer (paper Sec. 3.2, Eq. 2: span
+ * alpha + beta * N per head; clipping per Appendix "Main Setup").
+ * alpha, beta: host arrays of num_kv_heads finite doubles.  On success *out
+ * receives a new plan (free it with moa_plan_free).  Host only: runs without
+ * a GPU. */
+moa_status_t moa_plan(const moa_desc_t* desc, const double* alpha, const double* beta,
+                      moa_plan_t** out);
+
+/* Copies the plan's tables to caller-owned host arrays (any may be NULL):
+ * window[num_kv_heads], capacity[num_kv_heads], offset[num_kv_heads + 1]
+ * (offset[g] = sum of capacities of heads < g; offset[num_kv_heads] = R). */
+moa_status_t moa_plan_tables(const moa_plan_t* plan, int32_t* window, int32_t* capacity,
+                             int64_t* offset);
+
+/* Releases a plan (NULL is allowed). */
+void moa_plan_free(moa_plan_t* plan);
+
+/* Prefill attention (paper Sec. 2.1, Eq. 1, masked per KV head by the
+ * Sec. 3.2 span): for every batch b, query head h and position i < n_tokens,
+ *   o[b,i,h,:] = sum_{j visible to i} softmax_j(scale * q[b,i,h,:].k[b,j,g,:]) v[b,j,g,:]
+ * with g the KV head of h.  q, k, v, o: device pointers in the layouts above;
+ * o must not overlap the inputs.  Keys outside each head's sink prefix and
+ * band are never read.  batch >= 1, 1 <= n_tokens < 2^30. */
+moa_status_t moa_prefill(const moa_plan_t* plan, const void* q, const void* k, const void* v,
+                         void* o, int32_t batch, int64_t n_tokens, void* hip_stream);
+
+/* Appends positions start_pos .. start_pos + n_new - 1 of every sequence to
+ * the per-head static caches (paper Appendix "Efficiency Experiment Setup":
+ * the oldest KV entry beyond the span is replaced by the latest).  k_new,
+ * v_new: device [batch, n_new, num_kv_heads, head_dim].  Only each slot's
+ * final occupant is written (K/V bits copied exactly, pos_cache set to the
+ * position), so one bulk append equals n_new single appends.  Protocol:
+ * appends start at 0 and are contiguous; all sequences of a batch share
+ * start_pos.  1 <= batch <= 65535, start_pos >= 0, n_new >= 1,
+ * start_pos + n_new < 2^31. */
+moa_status_t moa_kv_append(const moa_plan_t* plan, void* k_cache, void* v_cache,
+                           int32_t* pos_cache, const void* k_new, const void* v_new,
+                           int32_t batch, int64_t start_pos, int64_t n_new, void* hip_stream);
+
+/* Bytes of device workspace moa_decode needs for `batch` sequences (the
+ * maximum over all positions).  Returns 0 for a NULL plan or batch < 1. */
+size_t moa_decode_workspace_bytes(const moa_plan_t* plan, int32_t batch);
+
+/* Decode attention for the token at position `pos` of every sequence (paper
+ * Appendix "Efficiency Experiment Setup": one query against per-head caches
+ * of different lengths).  Must follow moa_kv_append(start_pos = pos,
+ * n_new = 1), so that each head's filled slots hold exactly the keys visible
+ * to position pos.  q, o: device [batch, num_q_heads, head_dim].
+ * workspace: device buffer of ws_bytes >= moa_decode_workspace_bytes(plan,
+ * batch), 256-byte aligned, zero-filled by the caller once before its first
+ * use; every call leaves it reusable (its counters back at zero).  Calls that
+ * share one workspace must be ordered on one stream. */
+moa_status_t moa_decode(const moa_plan_t* plan, const void* q, const void* k_cache,
+                        const void* v_cache, void* o, int32_t batch, int64_t pos,
+                        void* workspace, size_t ws_bytes, void* hip_stream);
+
+/* Thread-local message of the calling thread's last non-OK status ("" if none). */
+const char* moa_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOA_H_ */

@@ -1,0 +1,268 @@
+// Host side of the C ABI: plan construction, argument validation, error
+// reporting and dispatch to the HIP kernel launchers.  Compiled with
+// -ffp-contract=off so the elastic rule is evaluated exactly as written.
+#include <math.h>
+#include <string.h>
+
+#include <algorithm>
+#include <new>
+#include <numeric>
+#include <string>
+
+#include "moa_internal.h"
+
+namespace moa {
+
+static thread_local std::string g_last_error;
+
+moa_status_t fail(moa_status_t st, const std::string& msg) {
+  g_last_error = msg;
+  return st;
+}
+
+moa_status_t ok() { return MOA_OK; }
+
+static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+void decode_geometry(const moa_plan_s& p, int64_t pos, DecodeGeometry* g) {
+  const int hkv = p.desc.num_kv_heads;
+  g->item_start[0] = 0;
+  for (int h = 0; h < hkv; ++h) {
+    const int64_t fill = std::min<int64_t>(pos + 1, p.capacity[h]);
+    g->fill[h] = static_cast<int32_t>(fill);
+    g->item_start[h + 1] = g->item_start[h] + static_cast<int32_t>(ceil_div(fill, p.decode_chunk));
+  }
+  g->items_per_seq = g->item_start[hkv];
+}
+
+// Workspace layout: [counters int32 batch*hkv, padded to 256 B][partials fp32].
+size_t decode_partials_offset(const moa_plan_s& p, int32_t batch) {
+  const size_t counters = sizeof(int32_t) * static_cast<size_t>(batch) * p.desc.num_kv_heads;
+  return (counters + 255) / 256 * 256;
+}
+
+static size_t decode_workspace_bytes(const moa_plan_s& p, int32_t batch) {
+  int64_t max_items = 0;
+  for (int h = 0; h < p.desc.num_kv_heads; ++h) max_items += ceil_div(p.capacity[h], p.decode_chunk);
+  const size_t per_item = sizeof(float) * static_cast<size_t>(p.group) * (p.desc.head_dim + 2);
+  return decode_partials_offset(p, batch) + per_item * static_cast<size_t>(max_items) * batch;
+}
+
+static bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; }
+
+static bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+  const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+  return x < y + nb && y < x + na;
+}
+
+static size_t elem_size(const moa_plan_s& p) { return p.desc.dtype == MOA_BF16 ? 2 : 4; }
+
+}  // namespace moa
+
+using namespace moa;
+
+extern "C" {
+
+const char* moa_last_error(void) { return g_last_error.c_str(); }
+
+moa_status_t moa_plan(const moa_desc_t* desc, const double* alpha, const double* beta,
+                      moa_plan_t** out) {
+  if (!desc || !alpha || !beta || !out) return fail(MOA_ERR_INVALID_ARG, "moa_plan: null argument");
+  *out = nullptr;
+  const moa_desc_t d = *desc;
+  if (d.num_kv_heads < 1 || d.num_kv_heads > MOA_MAX_KV_HEADS)
+    return fail(MOA_ERR_INVALID_ARG, "moa_plan: num_kv_heads must be in [1, MOA_MAX_KV_HEADS]");
+  if (d.num_q_heads < 1 || d.num_q_heads > MOA_MAX_Q_HEADS)
+    return fail(MOA_ERR_INVALID_ARG, "moa_plan: num_q_heads must be in [1, MOA_MAX_Q_HEADS]");
+  if (d.num_q_heads % d.num_kv_heads != 0)
+    return fail(MOA_ERR_INVALID_ARG, "moa_plan: num_q_heads must be a multiple of num_kv_heads");
+  const int group = d.num_q_heads / d.num_kv_heads;
+  if (group != 1 && group != 2 && group != 4 && group != 8)
+    return fail(MOA_ERR_UNSUPPORTED, "moa_plan: query group size must be 1, 2, 4 or 8");
+  if (d.head_dim != 64 && d.head_dim != 128)
+    return fail(MOA_ERR_UNSUPPORTED, "moa_plan: head_dim must be 64 or 128");
+  if (d.num_sink < 0 || d.num_sink >= (1 << 30))
+    return fail(MOA_ERR_INVALID_ARG, "moa_plan: num_sink must be in [0, 2^30)");
+  if (d.n < 1 || d.n >= (int64_t(1) << 30))
+    return fail(MOA_ERR_INVALID_ARG, "moa_plan: n must be in [1, 2^30)");
+  if (d.dtype != MOA_F32 && d.dtype != MOA_BF16)
+    return fail(MOA_ERR_INVALID_ARG, "moa_plan: dtype must be MOA_F32 or MOA_BF16");
+  if (!isfinite(d.softmax_scale) || d.softmax_scale < 0.0f)
+    return fail(MOA_ERR_INVALID_ARG, "moa_plan: softmax_scale must be finite and >= 0");
+  for (int h = 0; h < d.num_kv_heads; ++h)
+    if (!isfinite(alpha[h]) || !isfinite(beta[h]))
+      return fail(MOA_ERR_INVALID_ARG, "moa_plan: alpha and beta must be finite");
+
+  moa_plan_s* p = new (std::nothrow) moa_plan_s();
+  if (!p) return fail(MOA_ERR_INVALID_ARG, "moa_plan: out of host memory");
+  p->desc = d;
+  p->group = group;
+  p->scale = d.softmax_scale > 0.0f ? d.softmax_scale : static_cast<float>(1.0 / sqrt(double(d.head_dim)));
+  p->decode_chunk = kDecodeChunk;
+  const int hkv = d.num_kv_heads;
+  p->window.resize(hkv);
+  p->capacity.resize(hkv);
+  p->offset.assign(hkv + 1, 0);
+  const double nd = static_cast<double>(d.n);
+  for (int h = 0; h < hkv; ++h) {
+    // Elastic rule alpha + beta * N (paper Sec. 3.2, Eq. 2), floored and clipped to [1, N].
+    volatile double prod = beta[h] * nd;   // separate rounding: no fused multiply-add
+    const double x = alpha[h] + prod;
+    int64_t w;
+    if (!(x >= 1.0)) w = 1;
+    else if (x >= nd) w = d.n;
+    else w = static_cast<int64_t>(floor(x));
+    p->window[h] = static_cast<int32_t>(w);
+    p->capacity[h] = static_cast<int32_t>(w + d.num_sink);
+    p->offset[h + 1] = p->offset[h] + p->capacity[h];
+  }
+  p->head_order.resize(d.num_q_heads);
+  std::iota(p->head_order.begin(), p->head_order.end(), 0);
+  std::stable_sort(p->head_order.begin(), p->head_order.end(), [&](int16_t a, int16_t b) {
+    return p->window[a / group] > p->window[b / group];
+  });
+  *out = p;
+  return ok();
+}
+
+moa_status_t moa_plan_tables(const moa_plan_t* plan, int32_t* window, int32_t* capacity,
+                             int64_t* offset) {
+  if (!plan) return fail(MOA_ERR_INVALID_ARG, "moa_plan_tables: null plan");
+  const int hkv = plan->desc.num_kv_heads;
+  if (window) memcpy(window, plan->window.data(), sizeof(int32_t) * hkv);
+  if (capacity) memcpy(capacity, plan->capacity.data(), sizeof(int32_t) * hkv);
+  if (offset) memcpy(offset, plan->offset.data(), sizeof(int64_t) * (hkv + 1));
+  return ok();
+}
+
+void moa_plan_free(moa_plan_t* plan) { delete plan; }
+
+moa_status_t moa_prefill(const moa_plan_t* plan, const void* q, const void* k, const void* v,
+                         void* o, int32_t batch, int64_t n_tokens, void* hip_stream) {
+  if (!plan) return fail(MOA_ERR_INVALID_ARG, "moa_prefill: null plan");
+  if (!q || !k || !v || !o) return fail(MOA_ERR_INVALID_ARG, "moa_prefill: null tensor pointer");
+  if (batch < 1) return fail(MOA_ERR_INVALID_ARG, "moa_prefill: batch must be >= 1");
+  if (n_tokens < 1 || n_tokens >= (int64_t(1) << 30))
+    return fail(MOA_ERR_INVALID_ARG, "moa_prefill: n_tokens must be in [1, 2^30)");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o))
+    return fail(MOA_ERR_INVALID_ARG, "moa_prefill: tensors must be 16-byte aligned");
+  const moa_desc_t& d = plan->desc;
+  const size_t es = elem_size(*plan);
+  const size_t qbytes = es * batch * n_tokens * d.num_q_heads * d.head_dim;
+  const size_t kbytes = es * batch * n_tokens * d.num_kv_heads * d.head_dim;
+  if (overlaps(o, qbytes, q, qbytes) || overlaps(o, qbytes, k, kbytes) || overlaps(o, qbytes, v, kbytes))
+    return fail(MOA_ERR_INVALID_ARG, "moa_prefill: output overlaps an input");
+  const int64_t tiles = (n_tokens + kPrefillRows - 1) / kPrefillRows;
+  if (tiles * batch * d.num_q_heads >= (int64_t(1) << 31))
+    return fail(MOA_ERR_UNSUPPORTED, "moa_prefill: too many work-groups for one launch");
+
+  PrefillArgs a;
+  memset(&a, 0, sizeof(a));
+  a.q = q; a.k = k; a.v = v; a.o = o;
+  a.n = n_tokens;
+  a.batch = batch;
+  a.hq = d.num_q_heads;
+  a.hkv = d.num_kv_heads;
+  a.group = plan->group;
+  a.num_sink = d.num_sink;
+  a.n_qtiles = static_cast<int32_t>(tiles);
+  a.scale_log2 = plan->scale * 1.4426950408889634f;
+  for (int h = 0; h < d.num_kv_heads; ++h) a.window[h] = plan->window[h];
+  for (int h = 0; h < d.num_q_heads; ++h) a.head_order[h] = plan->head_order[h];
+  const int err = launch_prefill(a, d.dtype, d.head_dim, hip_stream);
+  if (err) return fail(MOA_ERR_HIP, "moa_prefill: kernel launch failed (hipError " + std::to_string(err) + ")");
+  return ok();
+}
+
+moa_status_t moa_kv_append(const moa_plan_t* plan, void* k_cache, void* v_cache,
+                           int32_t* pos_cache, const void* k_new, const void* v_new,
+                           int32_t batch, int64_t start_pos, int64_t n_new, void* hip_stream) {
+  if (!plan) return fail(MOA_ERR_INVALID_ARG, "moa_kv_append: null plan");
+  if (!k_cache || !v_cache || !pos_cache || !k_new || !v_new)
+    return fail(MOA_ERR_INVALID_ARG, "moa_kv_append: null tensor pointer");
+  if (batch < 1 || batch > 65535) return fail(MOA_ERR_INVALID_ARG, "moa_kv_append: batch must be in [1, 65535]");
+  if (start_pos < 0 || n_new < 1 || start_pos + n_new >= (int64_t(1) << 31))
+    return fail(MOA_ERR_INVALID_ARG, "moa_kv_append: need start_pos >= 0, n_new >= 1, start_pos + n_new < 2^31");
+  if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(k_new) || !aligned16(v_new) ||
+      (reinterpret_cast<uintptr_t>(pos_cache) & 3u))
+    return fail(MOA_ERR_INVALID_ARG, "moa_kv_append: tensors must be 16-byte aligned (pos_cache 4-byte)");
+  const moa_desc_t& d = plan->desc;
+  AppendArgs a;
+  memset(&a, 0, sizeof(a));
+  a.kc = k_cache; a.vc = v_cache; a.pos = pos_cache; a.kn = k_new; a.vn = v_new;
+  a.rows_total = plan->offset[d.num_kv_heads];
+  a.start = start_pos;
+  a.end = start_pos + n_new;
+  a.batch = batch;
+  a.hkv = d.num_kv_heads;
+  a.num_sink = d.num_sink;
+  a.cand_start[0] = 0;
+  const int64_t s = d.num_sink;
+  for (int h = 0; h < d.num_kv_heads; ++h) {
+    // Final occupants: sink positions in [start, min(end, s)) and the last
+    // w_h positions >= s, i.e. [max(start, s, end - w_h), end).
+    const int64_t w = plan->window[h];
+    const int64_t n_sink = std::max<int64_t>(0, std::min<int64_t>(a.end, s) - start_pos);
+    const int64_t lo = std::max<int64_t>(std::max<int64_t>(start_pos, s), a.end - w);
+    const int64_t n_band = std::max<int64_t>(0, a.end - lo);
+    a.cand_start[h + 1] = a.cand_start[h] + static_cast<int32_t>(n_sink + n_band);
+    a.window[h] = plan->window[h];
+    a.offset[h] = plan->offset[h];
+  }
+  a.rows_per_seq = a.cand_start[d.num_kv_heads];
+  if (static_cast<int64_t>(a.rows_per_seq) * batch * 64 >= (int64_t(1) << 31))
+    return fail(MOA_ERR_UNSUPPORTED, "moa_kv_append: too many rows for one launch");
+  const int err = launch_kv_append(a, d.dtype, d.head_dim, hip_stream);
+  if (err) return fail(MOA_ERR_HIP, "moa_kv_append: kernel launch failed (hipError " + std::to_string(err) + ")");
+  return ok();
+}
+
+size_t moa_decode_workspace_bytes(const moa_plan_t* plan, int32_t batch) {
+  if (!plan || batch < 1) return 0;
+  return decode_workspace_bytes(*plan, batch);
+}
+
+moa_status_t moa_decode(const moa_plan_t* plan, const void* q, const void* k_cache,
+                        const void* v_cache, void* o, int32_t batch, int64_t pos,
+                        void* workspace, size_t ws_bytes, void* hip_stream) {
+  if (!plan) return fail(MOA_ERR_INVALID_ARG, "moa_decode: null plan");
+  if (!q || !k_cache || !v_cache || !o) return fail(MOA_ERR_INVALID_ARG, "moa_decode: null tensor pointer");
+  if (batch < 1) return fail(MOA_ERR_INVALID_ARG, "moa_decode: batch must be >= 1");
+  if (pos < 0 || pos >= (int64_t(1) << 31) - 1)
+    return fail(MOA_ERR_INVALID_ARG, "moa_decode: pos must be in [0, 2^31 - 1)");
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(o))
+    return fail(MOA_ERR_INVALID_ARG, "moa_decode: tensors must be 16-byte aligned");
+  const size_t need = decode_workspace_bytes(*plan, batch);
+  if (!workspace || ws_bytes < need)
+    return fail(MOA_ERR_WORKSPACE, "moa_decode: workspace missing or smaller than moa_decode_workspace_bytes (" +
+                                       std::to_string(need) + " bytes)");
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u)
+    return fail(MOA_ERR_WORKSPACE, "moa_decode: workspace must be 256-byte aligned");
+  const moa_desc_t& d = plan->desc;
+  DecodeGeometry geo;
+  decode_geometry(*plan, pos, &geo);
+  if (static_cast<int64_t>(geo.items_per_seq) * batch >= (int64_t(1) << 31))
+    return fail(MOA_ERR_UNSUPPORTED, "moa_decode: too many work items for one launch");
+  DecodeArgs a;
+  memset(&a, 0, sizeof(a));
+  a.q = q; a.kc = k_cache; a.vc = v_cache; a.o = o;
+  a.counters = static_cast<int32_t*>(workspace);
+  a.part = reinterpret_cast<float*>(static_cast<char*>(workspace) + decode_partials_offset(*plan, batch));
+  a.rows_total = plan->offset[d.num_kv_heads];
+  a.batch = batch;
+  a.hq = d.num_q_heads;
+  a.hkv = d.num_kv_heads;
+  a.chunk = plan->decode_chunk;
+  a.items_per_seq = geo.items_per_seq;
+  a.scale_log2 = plan->scale * 1.4426950408889634f;
+  for (int h = 0; h < d.num_kv_heads; ++h) {
+    a.fill[h] = geo.fill[h];
+    a.offset[h] = plan->offset[h];
+  }
+  for (int h = 0; h <= d.num_kv_heads; ++h) a.item_start[h] = geo.item_start[h];
+  const int err = launch_decode(a, d.dtype, d.head_dim, plan->group, hip_stream);
+  if (err) return fail(MOA_ERR_HIP, "moa_decode: kernel launch failed (hipError " + std::to_string(err) + ")");
+  return ok();
+}
+
+}  // extern "C"

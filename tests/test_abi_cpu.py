@@ -1,0 +1,165 @@
+"""C-ABI checks that need no GPU: exported symbols, plan tables, error paths.
+
+Only host-side calls are made here (moa_plan and argument validation, which
+returns before any launch).
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from conftest import ROOT
+import oracle
+from paper_2406_14909_amd import moa as M
+
+lib = M.load_library()
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "moa.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(moa_[a-z_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = declared_functions()
+    assert set(names) == set(M.EXPORTED)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_desc_struct_layout_matches_header():
+    assert ctypes.sizeof(M.moa_desc_t) == 32
+    assert M.moa_desc_t.n.offset == 16 and M.moa_desc_t.softmax_scale.offset == 28
+
+
+def _plan(alpha, beta, n, s=64, hq=None, hkv=None, d=128, dtype="bf16"):
+    hkv = hkv or len(alpha)
+    return M.moa_plan(hq or hkv, hkv, d, s, n, dtype, alpha, beta)
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_plan_tables_equal_oracle_plan_bit_exact(seed):
+    rng = np.random.default_rng(seed)
+    hkv = int(rng.integers(1, 65))
+    n = int(rng.integers(1, 1 << 20))
+    s = int(rng.integers(0, 200))
+    alpha = rng.uniform(-2048, 8192, hkv)
+    beta = rng.uniform(0, 1, hkv)
+    # exact edge values in the sampled domain
+    alpha[: min(hkv, 4)] = [-2048.0, 0.0, 8192.0, 64.5][: min(hkv, 4)]
+    p = _plan(alpha, beta, n, s)
+    ref = oracle.plan_ref(alpha, beta, n, s)
+    assert np.array_equal(p.window, ref["window"])
+    assert np.array_equal(p.capacity, ref["capacity"])
+    assert np.array_equal(p.offset, ref["offset"])
+    assert p.cache_rows == int(ref["offset"][-1])
+
+
+def test_plan_rounding_edges():
+    # values whose floor is sensitive to rounding of alpha + beta * N
+    n = 3
+    alpha = [0.1, 1.0 - 2 ** -52, 2.0, -0.0, 1e300, -1e300]
+    beta = [0.3, 0.0, 1.0 / 3.0, 0.5, 0.0, 1.0]
+    p = _plan(alpha, beta, n, 0, d=64, dtype="f32")
+    ref = oracle.plan_ref(alpha, beta, n, 0)
+    assert np.array_equal(p.window, ref["window"])
+
+
+def test_workload_plans_match_oracle():
+    import workloads
+    for wl in workloads.workloads():
+        p = M.moa_plan(wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.num_sink, wl.n, wl.dtype,
+                       wl.alpha, wl.beta)
+        ref = oracle.plan_ref(wl.alpha, wl.beta, wl.n, wl.num_sink)
+        assert np.array_equal(p.window, ref["window"]), wl.name
+        assert np.array_equal(p.offset, ref["offset"]), wl.name
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(hkv=0), M.MOA_ERR_INVALID_ARG),
+    (dict(hkv=65), M.MOA_ERR_INVALID_ARG),
+    (dict(hq=6, hkv=4), M.MOA_ERR_INVALID_ARG),
+    (dict(hq=12, hkv=4), M.MOA_ERR_UNSUPPORTED),
+    (dict(hq=64, hkv=4), M.MOA_ERR_UNSUPPORTED),
+    (dict(d=96), M.MOA_ERR_UNSUPPORTED),
+    (dict(s=-1), M.MOA_ERR_INVALID_ARG),
+    (dict(n=0), M.MOA_ERR_INVALID_ARG),
+    (dict(n=1 << 30), M.MOA_ERR_INVALID_ARG),
+    (dict(dtype=7), M.MOA_ERR_INVALID_ARG),
+    (dict(scale=-1.0), M.MOA_ERR_INVALID_ARG),
+    (dict(scale=float("nan")), M.MOA_ERR_INVALID_ARG),
+    (dict(alpha=float("inf")), M.MOA_ERR_INVALID_ARG),
+    (dict(beta=float("nan")), M.MOA_ERR_INVALID_ARG),
+])
+def test_plan_rejects_invalid_descriptors(kw, status):
+    hkv = kw.get("hkv", 4)
+    desc = M.moa_desc_t(kw.get("hq", hkv), hkv, kw.get("d", 128), kw.get("s", 4), kw.get("n", 512),
+                        kw.get("dtype", M.MOA_BF16), kw.get("scale", 0.0))
+    m = max(hkv, 1)
+    a = (ctypes.c_double * m)(*([kw.get("alpha", 16.0)] * m))
+    b = (ctypes.c_double * m)(*([kw.get("beta", 0.5)] * m))
+    out = ctypes.c_void_p(1)
+    assert lib.moa_plan(ctypes.byref(desc), a, b, ctypes.byref(out)) == status
+    assert out.value is None
+    assert lib.moa_last_error().decode().startswith("moa_plan")
+
+
+def test_plan_null_arguments():
+    out = ctypes.c_void_p()
+    assert lib.moa_plan(None, None, None, ctypes.byref(out)) == M.MOA_ERR_INVALID_ARG
+    assert lib.moa_plan_tables(None, None, None, None) == M.MOA_ERR_INVALID_ARG
+    lib.moa_plan_free(None)
+    assert lib.moa_decode_workspace_bytes(None, 4) == 0
+
+
+def test_gpu_entry_points_validate_before_launch():
+    # Every call below is invalid and must return before touching the GPU.
+    p = _plan([100.0, 200.0], [0.0, 0.0], 1024, 4, hq=4, hkv=2)
+    h = p.handle
+    fake = 1 << 20          # aligned non-null address, never dereferenced
+    st = lib.moa_prefill(h, None, fake, fake, fake, 1, 16, None)
+    assert st == M.MOA_ERR_INVALID_ARG and "null" in lib.moa_last_error().decode()
+    assert lib.moa_prefill(None, fake, fake, fake, fake, 1, 16, None) == M.MOA_ERR_INVALID_ARG
+    assert lib.moa_prefill(h, fake, fake, fake, fake + 1 << 30, 0, 16, None) == M.MOA_ERR_INVALID_ARG
+    assert lib.moa_prefill(h, fake, fake, fake, fake, 1, 0, None) == M.MOA_ERR_INVALID_ARG
+    assert lib.moa_prefill(h, fake + 8, fake, fake, fake, 1, 16, None) == M.MOA_ERR_INVALID_ARG
+    st = lib.moa_prefill(h, fake, 2 * fake, 3 * fake, fake + 64, 1, 16, None)
+    assert st == M.MOA_ERR_INVALID_ARG and "overlap" in lib.moa_last_error().decode()
+
+    assert lib.moa_kv_append(h, fake, fake, fake, None, fake, 1, 0, 1, None) == M.MOA_ERR_INVALID_ARG
+    assert lib.moa_kv_append(h, fake, fake, fake, fake, fake, 0, 0, 1, None) == M.MOA_ERR_INVALID_ARG
+    assert lib.moa_kv_append(h, fake, fake, fake, fake, fake, 70000, 0, 1, None) == M.MOA_ERR_INVALID_ARG
+    assert lib.moa_kv_append(h, fake, fake, fake, fake, fake, 1, -1, 1, None) == M.MOA_ERR_INVALID_ARG
+    assert lib.moa_kv_append(h, fake, fake, fake, fake, fake, 1, 0, 0, None) == M.MOA_ERR_INVALID_ARG
+    assert lib.moa_kv_append(h, fake, fake, fake, fake, fake, 1, (1 << 31) - 1, 1, None) == M.MOA_ERR_INVALID_ARG
+    assert lib.moa_kv_append(h, fake, fake, fake + 2, fake, fake, 1, 0, 1, None) == M.MOA_ERR_INVALID_ARG
+
+    need = lib.moa_decode_workspace_bytes(h, 2)
+    assert need > 0
+    assert lib.moa_decode(h, fake, fake, fake, fake, 2, 0, None, need, None) == M.MOA_ERR_WORKSPACE
+    assert lib.moa_decode(h, fake, fake, fake, fake, 2, 0, fake, need - 1, None) == M.MOA_ERR_WORKSPACE
+    assert lib.moa_decode(h, fake, fake, fake, fake, 2, 0, fake + 16, need, None) == M.MOA_ERR_WORKSPACE
+    assert lib.moa_decode(h, fake, fake, fake, fake, 2, -1, fake, need, None) == M.MOA_ERR_INVALID_ARG
+    assert lib.moa_decode(h, fake, fake, fake, fake, 0, 0, fake, need, None) == M.MOA_ERR_INVALID_ARG
+    assert lib.moa_decode(h, None, fake, fake, fake, 2, 0, fake, need, None) == M.MOA_ERR_INVALID_ARG
+
+
+def test_decode_workspace_grows_with_batch_and_capacity():
+    small = _plan([100.0, 200.0], [0.0, 0.0], 1024, 4, hq=4, hkv=2)
+    big = _plan([5000.0, 200.0], [0.0, 0.0], 8192, 4, hq=4, hkv=2)
+    assert M.moa_decode_workspace_bytes(small, 2) < M.moa_decode_workspace_bytes(small, 8)
+    assert M.moa_decode_workspace_bytes(small, 2) < M.moa_decode_workspace_bytes(big, 2)
+
+
+def test_binding_fails_loudly_without_library(tmp_path):
+    import importlib
+    saved = M._lib
+    try:
+        M._lib = None
+        with pytest.raises(ImportError):
+            M.load_library(str(tmp_path / "missing.so"))
+    finally:
+        M._lib = saved

@@ -1,0 +1,113 @@
+"""GPU parity at the full workload sizes, on sampled outputs the oracle computes row by row.
+
+Shapes are those of the five named workloads (Vicuna-7B / Llama3-8B /
+Llama3-70B-shaped layers, bf16, 64 sinks, elastic windows), launched exactly
+as the benchmark launches them.  Sampled rows cover the sink region, both
+sides of every head's window edge, the band interior, the last rows and
+seeded random rows.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from helpers import assert_close
+from paper_2406_14909_amd import moa as M
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print("[case]", *a, flush=True)
+
+
+def _sample_rows(n, w, s, rng, extra=6):
+    cand = {0, 1, s - 1, s, s + 1, w - 2, w - 1, w, w + 1, w + s, n // 2, n - 129, n - 2, n - 1}
+    cand |= set(int(x) for x in rng.integers(0, n, extra))
+    return sorted(x for x in cand if 0 <= x < n)
+
+
+def _check_prefill_rows(wl, q, k, v, o, plan, b_list, heads, rng):
+    group = wl.num_q_heads // wl.num_kv_heads
+    worst = 0.0
+    for b in b_list:
+        for h in heads:
+            g = h // group
+            rows = _sample_rows(int(q.shape[1]), int(plan.window[g]), wl.num_sink, rng)
+            qc = q[b:b + 1, :, h:h + 1].cpu()
+            kc = k[b:b + 1, :, g:g + 1].cpu()
+            vc = v[b:b + 1, :, g:g + 1].cpu()
+            ref = oracle.attention_rows_ref(qc, kc, vc, [int(plan.window[g])], wl.num_sink, 0, 0, rows)
+            got = o[b, rows, h].cpu()
+            worst = max(worst, assert_close(got, ref, torch.bfloat16, what=f"{wl.name} b={b} h={h}"))
+    return worst
+
+
+@pytest.mark.parametrize("idx", [1, 3, 4])
+def test_prefill_workload_sampled(idx):
+    wl = workloads.workload(idx)
+    bsz, n = wl.prefill_batch, wl.n
+    _say("prefill", wl.name, f"B={bsz} n={n}")
+    plan = M.moa_plan(wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.num_sink, n, wl.dtype,
+                      wl.alpha, wl.beta)
+    q = workloads.randn((bsz, n, wl.num_q_heads, wl.head_dim), 1000 + idx, torch.bfloat16, "cuda")
+    k = workloads.randn((bsz, n, wl.num_kv_heads, wl.head_dim), 2000 + idx, torch.bfloat16, "cuda")
+    v = workloads.randn((bsz, n, wl.num_kv_heads, wl.head_dim), 3000 + idx, torch.bfloat16, "cuda")
+    o = M.moa_prefill(plan, q, k, v)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(idx)
+    heads = list(range(wl.num_q_heads)) if wl.num_q_heads <= 32 else list(range(0, wl.num_q_heads, 3))
+    worst = _check_prefill_rows(wl, q, k, v, o, plan, [0], heads, rng)
+    _say("max err", worst)
+
+
+@pytest.mark.parametrize("idx", [2, 3, 4])
+def test_decode_workload_sampled(idx):
+    """Bulk-fills the caches from a context of N tokens, then runs decode steps
+    (append + decode) in the benchmark's launch configuration and checks
+    sampled (sequence, head) outputs of the first, a middle and the last step."""
+    wl = workloads.workload(idx)
+    bsz, n, steps = wl.decode_batch, wl.n, 3
+    _say("decode", wl.name, f"B={bsz} N={n}")
+    plan = M.moa_plan(wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.num_sink, n, wl.dtype,
+                      wl.alpha, wl.beta)
+    total = n + steps
+    k = workloads.randn((bsz, total, wl.num_kv_heads, wl.head_dim), 4000 + idx, torch.bfloat16, "cuda")
+    v = workloads.randn((bsz, total, wl.num_kv_heads, wl.head_dim), 5000 + idx, torch.bfloat16, "cuda")
+    q = workloads.randn((steps, bsz, wl.num_q_heads, wl.head_dim), 6000 + idx, torch.bfloat16, "cuda")
+    kc, vc, pos = M.new_cache(plan, bsz)
+    ws = M.new_workspace(plan, bsz)
+    M.moa_kv_append(plan, kc, vc, pos, k[:, :n].contiguous(), v[:, :n].contiguous(), 0)
+    outs = []
+    for i in range(steps):
+        t = n + i
+        M.moa_kv_append(plan, kc, vc, pos, k[:, t:t + 1].contiguous(), v[:, t:t + 1].contiguous(), t)
+        outs.append(M.moa_decode(plan, q[i], kc, vc, t, ws))
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(idx)
+    group = wl.num_q_heads // wl.num_kv_heads
+    b_list = sorted({0, bsz - 1, int(rng.integers(0, bsz))})
+    worst = 0.0
+    for b in b_list:
+        for g in range(wl.num_kv_heads):
+            kb = k[b:b + 1, :, g:g + 1].cpu()
+            vb = v[b:b + 1, :, g:g + 1].cpu()
+            for i in range(steps):
+                t = n + i
+                for h in range(g * group, (g + 1) * group):
+                    qt = q[i, b:b + 1, h:h + 1].cpu()
+                    ref = oracle.decode_ref(qt, kb[:, : t + 1], vb[:, : t + 1], [int(plan.window[g])],
+                                            wl.num_sink)
+                    got = outs[i][b:b + 1, h:h + 1]
+                    worst = max(worst, assert_close(got, ref, torch.bfloat16,
+                                                    what=f"{wl.name} t={t} b={b} h={h}"))
+    # the cache holds exactly the visible set of the newest token
+    last = n + steps - 1
+    for b in b_list:
+        p = pos[b].cpu().numpy()
+        for g in range(wl.num_kv_heads):
+            seg = p[plan.offset[g]:plan.offset[g + 1]]
+            got = sorted(int(x) for x in seg if x >= 0)
+            assert got == list(oracle.visible_set(last, int(plan.window[g]), wl.num_sink))
+    _say("max err", worst)
