@@ -179,7 +179,7 @@ def main() -> int:
         "prefill_ms": round(pre_ms, 4),
         "prefill_inband_tflops": round(pre_tflops, 2),
         "roofline": {
-            "kernel": "decode_kernel<bf16,128,1>",
+            "kernel": "moa_decode (decode_kernel<bf16,128,1> + decode_combine_kernel), per call",
             "bound": "hbm",
             "achieved": round(dec_gbs, 1),
             "peak": HBM_PEAK_GBS,
@@ -189,7 +189,7 @@ def main() -> int:
             "bytes_per_launch": round(dec_bytes_total / steps_dec),
         },
         "roofline_prefill": {
-            "kernel": "prefill_kernel<bf16,128>",
+            "kernel": "prefill_kernel<bf16,128>, per call",
             "bound": "mfma",
             "achieved": round(pre_tflops, 2),
             "peak": BF16_MFMA_PEAK_TFLOPS,

@@ -154,9 +154,11 @@ size_t moa_decode_workspace_bytes(const moa_plan_t* plan, int32_t batch);
  * n_new = 1), so that each head's filled slots hold exactly the keys visible
  * to position pos.  q, o: device [batch, num_q_heads, head_dim].
  * workspace: device buffer of ws_bytes >= moa_decode_workspace_bytes(plan,
- * batch), 256-byte aligned, zero-filled by the caller once before its first
- * use; every call leaves it reusable (its counters back at zero).  Calls that
- * share one workspace must be ordered on one stream. */
+ * batch), 256-byte aligned, holding split-K partial results; its contents
+ * need no initialisation and are meaningless after the call.  Calls that
+ * share one workspace must be ordered on one stream.  Launches one kernel, or
+ * two when some head's cache spans several split-K chunks (the second merges
+ * the chunks' partial results). */
 moa_status_t moa_decode(const moa_plan_t* plan, const void* q, const void* k_cache,
                         const void* v_cache, void* o, int32_t batch, int64_t pos,
                         void* workspace, size_t ws_bytes, void* hip_stream);

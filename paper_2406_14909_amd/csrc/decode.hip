@@ -12,9 +12,10 @@
 // head, so each K/V byte is read from HBM once.  Work-groups stream K/V with
 // 16-byte loads (LPR lanes cover one row), keep an online softmax per lane
 // group (base-2 exponent, scale folded into q), merge lane groups and waves,
-// and either write o directly (single chunk) or a partial (m, l, acc).  The
-// last work-group to finish a (sequence, KV head) - detected with an arrival
-// counter - merges the partials and writes o, then resets the counter.
+// and either write o directly (single chunk) or a partial (m, l, acc).  A
+// second, small kernel merges the partials of multi-chunk caches; the kernel
+// boundary makes the partials visible across the chip's L2 slices without
+// any in-kernel cache maintenance.
 #include "moa_device.h"
 
 namespace moa {
@@ -33,7 +34,6 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
 
   __shared__ float s_acc[kWaves][G][D];
   __shared__ float s_ml[kWaves][G][2];
-  __shared__ int s_last;
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -171,39 +171,31 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
       }
     }
   }
+}
+
+// Merges the split-K partials of every (sequence, KV head) with more than one
+// chunk: o = sum_c 2^(m_c - M) acc_c / sum_c 2^(m_c - M) l_c, M = max_c m_c.
+template <typename T, int D, int G>
+__global__ void __launch_bounds__(256) decode_combine_kernel(DecodeArgs a) {
+  const int b = blockIdx.x / a.hkv;
+  const int g = blockIdx.x - b * a.hkv;
+  const int nchunk = a.item_start[g + 1] - a.item_start[g];
   if (nchunk == 1) return;
-
-  // Arrival counter: the last chunk of this (sequence, KV head) merges.
-  __threadfence();
-  __syncthreads();
-  int32_t* counter = a.counters + int64_t(b) * a.hkv + g;
-  if (threadIdx.x == 0) {
-    const int prev = atomicAdd(counter, 1);
-    s_last = (prev == nchunk - 1) ? 1 : 0;
-  }
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-
   const int64_t first = int64_t(b) * a.items_per_seq + a.item_start[g];
   for (int idx = threadIdx.x; idx < G * D; idx += blockDim.x) {
     const int h = idx / D, d = idx % D;
     float mx = kNegBig;
-    for (int cc = 0; cc < nchunk; ++cc) {
-      const float* pp = a.part + ((first + cc) * G + h) * (D + 2);
-      mx = fmaxf(mx, __builtin_nontemporal_load(pp + D));
-    }
+    for (int cc = 0; cc < nchunk; ++cc) mx = fmaxf(mx, a.part[((first + cc) * G + h) * (D + 2) + D]);
     float lsum = 0.0f, asum = 0.0f;
     for (int cc = 0; cc < nchunk; ++cc) {
       const float* pp = a.part + ((first + cc) * G + h) * (D + 2);
-      const float f = fast_exp2(__builtin_nontemporal_load(pp + D) - mx);
-      lsum += __builtin_nontemporal_load(pp + D + 1) * f;
-      asum += __builtin_nontemporal_load(pp + d) * f;
+      const float f = fast_exp2(pp[D] - mx);
+      lsum += pp[D + 1] * f;
+      asum += pp[d] * f;
     }
     T* op = static_cast<T*>(a.o) + (int64_t(b) * a.hq + g * G + h) * D + d;
     *op = static_cast<T>(asum / lsum);
   }
-  if (threadIdx.x == 0) __hip_atomic_store(counter, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 template <typename T, int D, int G>
@@ -211,9 +203,14 @@ int launch_t(const DecodeArgs& a, void* stream) {
   const int64_t blocks = int64_t(a.batch) * a.items_per_seq;
   DecodeArgs copy = a;
   void* args[] = {&copy};
-  return static_cast<int>(hipLaunchKernel(reinterpret_cast<const void*>(&decode_kernel<T, D, G>),
-                                          dim3(static_cast<unsigned>(blocks)), dim3(256), args, 0,
-                                          static_cast<hipStream_t>(stream)));
+  hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(&decode_kernel<T, D, G>),
+                                 dim3(static_cast<unsigned>(blocks)), dim3(256), args, 0,
+                                 static_cast<hipStream_t>(stream));
+  if (e != hipSuccess || blocks == int64_t(a.batch) * a.hkv) return static_cast<int>(e);  // no split
+  e = hipLaunchKernel(reinterpret_cast<const void*>(&decode_combine_kernel<T, D, G>),
+                      dim3(static_cast<unsigned>(a.batch * a.hkv)), dim3(256), args, 0,
+                      static_cast<hipStream_t>(stream));
+  return static_cast<int>(e);
 }
 
 template <typename T, int D>

@@ -35,17 +35,14 @@ void decode_geometry(const moa_plan_s& p, int64_t pos, DecodeGeometry* g) {
   g->items_per_seq = g->item_start[hkv];
 }
 
-// Workspace layout: [counters int32 batch*hkv, padded to 256 B][partials fp32].
-size_t decode_partials_offset(const moa_plan_s& p, int32_t batch) {
-  const size_t counters = sizeof(int32_t) * static_cast<size_t>(batch) * p.desc.num_kv_heads;
-  return (counters + 255) / 256 * 256;
-}
-
+// Workspace: split-K partials, fp32 [batch * items][group][head_dim + 2]
+// (acc[head_dim], running max m, running sum l), sized for the largest
+// number of work items (every cache full).
 static size_t decode_workspace_bytes(const moa_plan_s& p, int32_t batch) {
   int64_t max_items = 0;
   for (int h = 0; h < p.desc.num_kv_heads; ++h) max_items += ceil_div(p.capacity[h], p.decode_chunk);
   const size_t per_item = sizeof(float) * static_cast<size_t>(p.group) * (p.desc.head_dim + 2);
-  return decode_partials_offset(p, batch) + per_item * static_cast<size_t>(max_items) * batch;
+  return per_item * static_cast<size_t>(max_items) * batch;
 }
 
 static bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; }
@@ -246,8 +243,7 @@ moa_status_t moa_decode(const moa_plan_t* plan, const void* q, const void* k_cac
   DecodeArgs a;
   memset(&a, 0, sizeof(a));
   a.q = q; a.kc = k_cache; a.vc = v_cache; a.o = o;
-  a.counters = static_cast<int32_t*>(workspace);
-  a.part = reinterpret_cast<float*>(static_cast<char*>(workspace) + decode_partials_offset(*plan, batch));
+  a.part = static_cast<float*>(workspace);
   a.rows_total = plan->offset[d.num_kv_heads];
   a.batch = batch;
   a.hq = d.num_q_heads;

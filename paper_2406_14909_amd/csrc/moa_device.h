@@ -56,11 +56,26 @@ __device__ __forceinline__ Vec16<T> zero16() {
   return r;
 }
 
-// Sum over aligned groups of `width` lanes (width a power of two <= 64).
+// DPP lane permutation of a float (no LDS round trip).
+template <int ctrl>
+__device__ __forceinline__ float dpp(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), ctrl, 0xF, 0xF, false));
+}
+
+// Sum over aligned groups of `width` lanes (width a power of two <= 64); every
+// lane of a group receives the group's sum.  Within 16 lanes the reduction uses
+// DPP: quad_perm [1,0,3,2] and [2,3,0,1] give quad sums, then row_half_mirror
+// and row_mirror exchange whole quads and half-rows (valid because the values
+// are already uniform across each quad / half-row at that point).
 template <int width>
 __device__ __forceinline__ float group_sum(float x) {
-#pragma unroll
-  for (int off = width / 2; off >= 1; off /= 2) x += __shfl_xor(x, off, 64);
+  static_assert(width >= 1 && width <= 64 && (width & (width - 1)) == 0, "width");
+  if constexpr (width >= 2) x += dpp<0xB1>(x);
+  if constexpr (width >= 4) x += dpp<0x4E>(x);
+  if constexpr (width >= 8) x += dpp<0x141>(x);
+  if constexpr (width >= 16) x += dpp<0x140>(x);
+  if constexpr (width >= 32) x += __shfl_xor(x, 16, 64);
+  if constexpr (width >= 64) x += __shfl_xor(x, 32, 64);
   return x;
 }
 

@@ -35,7 +35,6 @@ struct DecodeGeometry {
   int32_t items_per_seq;
 };
 void decode_geometry(const moa_plan_s& p, int64_t pos, DecodeGeometry* g);
-size_t decode_partials_offset(const moa_plan_s& p, int32_t batch);
 
 // ---------------------------------------------------------------------------
 // Kernel argument blocks (passed by value; the per-head tables ride along).
@@ -81,7 +80,6 @@ struct DecodeArgs {
   const void* vc;
   void* o;
   float* part;               // [items][group][D + 2] split-K partials
-  int32_t* counters;         // [batch * hkv] arrival counters (left at zero)
   int64_t rows_total;        // cache rows per sequence
   int32_t batch;
   int32_t hq;

@@ -219,10 +219,10 @@ def moa_decode_workspace_bytes(plan: Plan, batch: int) -> int:
 
 
 def new_workspace(plan: Plan, batch: int, device="cuda"):
-    """Zero-filled decode workspace of the required size."""
+    """Decode workspace of the required size (contents need no initialisation)."""
     import torch
     nbytes = max(256, moa_decode_workspace_bytes(plan, batch))
-    return torch.zeros(nbytes, dtype=torch.uint8, device=device)
+    return torch.empty(nbytes, dtype=torch.uint8, device=device)
 
 
 def moa_decode(plan: Plan, q, k_cache, v_cache, pos: int, workspace, o=None, stream=None):

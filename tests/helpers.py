@@ -10,7 +10,7 @@ F32_ATOL = 1e-5
 BF16_ATOL = 1e-2
 BF16_ROUND_REL = 2.0 ** -8
 
-SENTINEL = 12345.0
+SENTINEL = 12288.0   # exactly representable in bf16 and fp32
 
 
 def assert_close(gpu, ref, dtype, with_rounding=False, what=""):
@@ -40,8 +40,8 @@ def guarded_empty(shape, dtype, device="cuda", guard=4096):
 
 def guard_intact(buf, shape):
     n = int(np.prod(shape))
-    tail = buf[n:].float().cpu()
-    return bool(torch.all(tail == SENTINEL))
+    tail = buf[n:].cpu()
+    return bool(torch.all(tail == torch.tensor(SENTINEL, dtype=buf.dtype)))
 
 
 def bits(t):

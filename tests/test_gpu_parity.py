@@ -164,9 +164,8 @@ def _decode_run(dt, bsz, hq, hkv, d, s, windows, n0, steps, seed, poison=False):
     v = workloads.randn((bsz, total, hkv, d), seed + 2, dtype, "cuda")
     kc, vc, pos = M.new_cache(plan, bsz)
     ws = M.new_workspace(plan, bsz)
-    if poison:   # partials must never be read before being written
-        off = (bsz * hkv * 4 + 255) // 256 * 256
-        ws[off:].view(torch.uint8).fill_(0xFF)
+    if poison:   # partials must never be read before being written (0xFF.. = NaN)
+        ws.fill_(0xFF)
     M.moa_kv_append(plan, kc, vc, pos, k[:, :n0].contiguous(), v[:, :n0].contiguous(), 0)
     outs = []
     for t in range(n0, total):
@@ -179,8 +178,6 @@ def _decode_run(dt, bsz, hq, hkv, d, s, windows, n0, steps, seed, poison=False):
         assert guard_intact(buf, (bsz, hq, d)), f"write past decode output at {t}"
         ref = oracle.decode_ref(q[:, t], k[:, : t + 1], v[:, : t + 1], plan.window, s)
         assert_close(o, ref, dtype, with_rounding=True, what=f"decode t={t}")
-    # counters are left at zero for the next call
-    assert int(ws[: bsz * hkv * 4].view(torch.int32).abs().sum()) == 0
     return plan, q, k, v
 
 
