@@ -56,6 +56,19 @@ __device__ __forceinline__ Vec16<T> zero16() {
   return r;
 }
 
+// Direct global -> LDS copy of 16 bytes per lane (gfx950 global_load_lds_dwordx4):
+// lane i's bytes land at lds_base + 16 * i; lds_base must be wave-uniform.
+// The builtin is emitted only in the device pass (the host pass just needs the
+// kernel stubs and would otherwise drop some instantiations).
+__device__ __forceinline__ void dma16(const void* src, void* lds_base) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
+#else
+  (void)src;
+  (void)lds_base;
+#endif
+}
+
 // DPP lane permutation of a float (no LDS round trip).
 template <int ctrl>
 __device__ __forceinline__ float dpp(float x) {

@@ -5,20 +5,29 @@
 // One work-group = 4 waves = 128 query rows of one (sequence, query head);
 // each wave owns 32 rows.  The work-group walks only the 64-key tiles that
 // intersect the sink prefix or the band of its rows; every other tile is
-// skipped without being read.  K and V tiles are staged in LDS (V stored
-// transposed) and shared by the 4 waves.
+// skipped without being read.  K and V tiles are staged in LDS (double
+// buffered: the global loads of tile t+1 are in flight while tile t is
+// computed, one barrier per tile) and shared by the 4 waves.
 //
 // Matrix-core formulation (CDNA4 32x32 MFMA; bf16 32x32x16, fp32 32x32x2):
 //   S^T = K Q^T  : A = K tile rows (keys), B = Q^T kept in registers.
 //                  Output lane l holds the scores of query row l % 32 for
 //                  16 keys, so the row softmax needs one cross-lane step.
 //   O^T += V^T P^T : B = P^T taken straight from the score registers
-//                  (converted to the input type), A = V^T read from LDS.
+//                  (converted to the input type), A = V^T.  For bf16 the V
+//                  tile stays row-major in LDS and the transposing LDS read
+//                  (ds_read_b64_tr_b16) delivers V^T fragments; the fp32
+//                  instantiation stores V transposed instead.
 // The key order inside each 16-key MFMA step is permuted identically on both
 // operands, which leaves the sum unchanged.
-// Softmax is online (running max m and sum l per row) in base 2 with the
-// scale folded into the exponent; the mask is evaluated only on tiles that
-// are not entirely visible to the wave's rows.
+// Softmax is online in base 2 with the scale folded into one FMA per score
+// (bf16 instantiation).
+// The running maximum used as the exponent offset is raised only when some
+// row of the wave would otherwise see exponents above 2^8 (a wave-uniform
+// test), so most tiles skip rescaling the output accumulator; the final
+// normalisation by the running sum makes the result independent of that
+// offset.  The mask is evaluated only on tiles that are not entirely visible
+// to the wave's rows.
 #include "moa_device.h"
 
 namespace moa {
@@ -28,13 +37,14 @@ namespace {
 constexpr int BM = 128;   // query rows per work-group
 constexpr int BN = 64;    // keys per tile
 constexpr int NW = 4;     // waves per work-group
+constexpr float kRescaleSlack = 8.0f;   // log2 headroom before the offset is raised
+
+typedef short i16x4 __attribute__((ext_vector_type(4)));
 
 template <typename T> struct Mma;
 
 template <> struct Mma<bf16> {
   static constexpr int K = 16;                 // reduction depth per instruction
-  static constexpr int KPAD = 8;               // LDS row padding (elements)
-  static constexpr int VPAD = 4;
   typedef bf16x8 frag;
   __device__ __forceinline__ static f32x16 mma(const frag& a, const frag& b, const f32x16& c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -43,16 +53,13 @@ template <> struct Mma<bf16> {
 
 template <> struct Mma<float> {
   static constexpr int K = 2;
-  static constexpr int KPAD = 4;
-  static constexpr int VPAD = 4;
   typedef float frag;
   __device__ __forceinline__ static f32x16 mma(const frag& a, const frag& b, const f32x16& c) {
     return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
   }
 };
 
-// Fragment of K / Q for reduction step kk: row `row` of a [*, ld] array,
-// elements kk*K + (lane/32)*(K/2) ... (+K/2).
+// Fragment of K / Q for reduction step kk: elements kk*K + half*(K/2) ... (+K/2).
 __device__ __forceinline__ bf16x8 load_frag(const bf16* base, int kk, int half) {
   return *reinterpret_cast<const bf16x8*>(base + kk * 16 + half * 8);
 }
@@ -60,17 +67,60 @@ __device__ __forceinline__ float load_frag(const float* base, int kk, int half) 
   return base[kk * 2 + half];
 }
 
-template <typename T, int D>
-__global__ void __launch_bounds__(256) prefill_kernel(PrefillArgs a) {
-  using M = Mma<T>;
-  constexpr int KS = D / M::K;            // MFMA steps over the head dimension
-  constexpr int LDK = D + M::KPAD;        // LDS row stride of the K tile
-  constexpr int LDV = BN + M::VPAD;       // LDS row stride of the V^T tile
-  constexpr int EPL = Vec16<T>::N;        // elements per 16-byte load
-  constexpr int CPR = D / EPL;            // 16-byte chunks per row
+// Transposing LDS read of four bf16: within each 16-lane group, lane 4a+b
+// receives element b of the 8-byte reads issued by lanes 4e+a (e = 0..3).
+// (The builtin exists only in the device pass; the host pass, which merely
+// emits kernel stubs, sees an empty body.)
+__device__ __forceinline__ bf16x4 read_tr(const bf16* p) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  const i16x4 r = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (__attribute__((address_space(3))) i16x4*)(const_cast<bf16*>(p)));
+  return __builtin_bit_cast(bf16x4, r);
+#else
+  (void)p;
+  return bf16x4{};
+#endif
+}
 
-  __shared__ __attribute__((aligned(16))) T sK[BN * LDK];
-  __shared__ __attribute__((aligned(16))) T sV[D * LDV];
+// x * y - z with the product rounded on its own (never fused).
+__device__ __forceinline__ float mul_then_sub(float x, float y, float z) {
+#pragma clang fp contract(off)
+  return x * y - z;
+}
+
+template <typename T, int D>
+struct Tiles {
+  static constexpr bool kTr = sizeof(T) == 2;        // bf16: V via the transposing read
+  static constexpr int RB = D * int(sizeof(T));      // bytes per K/V row
+  static constexpr int CPR = RB / 16;                // 16-byte chunks per row
+  static constexpr int TILE_BYTES = BN * RB;         // one V tile (bf16, row-major)
+  // K rows carry one 16-byte padding chunk: stride RBP = RB + 16, so the rows
+  // read together by an MFMA operand load start in different bank groups.
+  static constexpr int RBP = RB + 16;
+  static constexpr int KCH = BN * (CPR + 1);         // 16-byte chunks in a padded K tile
+  static constexpr int K_DMA = (KCH + 63) / 64;      // 1 KB direct-to-LDS loads per K tile
+  static constexpr int K_BYTES = K_DMA * 1024;       // K buffer (slack after the last row)
+  static constexpr int V_DMA_PER_WAVE = TILE_BYTES / 1024 / NW;
+  static constexpr int EPL = Vec16<T>::N;            // elements per 16-byte chunk
+  static constexpr int VT_LD = BN + 4;               // fp32 only: V^T row stride (elements)
+  static constexpr int VT_BYTES = D * VT_LD * int(sizeof(T));
+  static constexpr int V_BYTES = kTr ? TILE_BYTES : VT_BYTES;
+  static constexpr int VREG = kTr ? 1 : BN * CPR / (NW * 64);   // fp32 V chunks staged per thread
+  // V rows (bf16): chunk c of row r sits at chunk position c ^ swz_v(r), which
+  // depends on r mod 8 only; the 4 rows x 4 chunks read by half a wave in one
+  // transposing load then hit 16 different bank groups.
+  __device__ __forceinline__ static int swz_v(int r) { return CPR >= 16 ? 4 * (r & 3) : 4 * ((r >> 1) & 1); }
+};
+
+template <typename T, int D>
+__global__ void __launch_bounds__(NW * 64, 2) prefill_kernel(PrefillArgs a) {
+  using M = Mma<T>;
+  using TL = Tiles<T, D>;
+  constexpr int KS = D / M::K;            // MFMA steps over the head dimension
+  constexpr int RB = TL::RB, RBP = TL::RBP, CPR = TL::CPR, EPL = TL::EPL;
+
+  __shared__ __attribute__((aligned(1024))) char sK[2][TL::K_BYTES];
+  __shared__ __attribute__((aligned(1024))) char sV[2][TL::V_BYTES];
 
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
@@ -88,6 +138,7 @@ __global__ void __launch_bounds__(256) prefill_kernel(PrefillArgs a) {
   const int64_t n = a.n;
   const int w = a.window[g];
   const int s = a.num_sink;
+  const float c2 = a.scale_log2;
 
   const int i0 = qt * BM;
   const int i1 = static_cast<int>(min(n, int64_t(i0 + BM)));   // exclusive
@@ -102,10 +153,10 @@ __global__ void __launch_bounds__(256) prefill_kernel(PrefillArgs a) {
   const int ntiles = ta + max(0, tl - tb + 1);
 
   const int64_t q_row_stride = int64_t(a.hq) * D;
-  const int64_t kv_row_stride = int64_t(a.hkv) * D;
+  const int64_t kv_row_bytes = int64_t(a.hkv) * RB;
   const T* qg = static_cast<const T*>(a.q) + (int64_t(b) * n * a.hq + h) * D;
-  const T* kg = static_cast<const T*>(a.k) + (int64_t(b) * n * a.hkv + g) * D;
-  const T* vg = static_cast<const T*>(a.v) + (int64_t(b) * n * a.hkv + g) * D;
+  const char* kg = static_cast<const char*>(a.k) + (int64_t(b) * n * a.hkv + g) * RB;
+  const char* vg = static_cast<const char*>(a.v) + (int64_t(b) * n * a.hkv + g) * RB;
 
   // Q^T fragments of this lane's query row (zeros past the end).
   typename M::frag qf[KS];
@@ -121,34 +172,89 @@ __global__ void __launch_bounds__(256) prefill_kernel(PrefillArgs a) {
     }
   }
 
+  // Direct-to-LDS tile loads: DMA instruction I writes buffer bytes
+  // [I*1024, I*1024 + 1024) and lane L's 16 bytes land at chunk I*64 + L.
+  // K: chunk m is row m / (CPR+1), column chunk m % (CPR+1); the last column
+  // chunk of each row (and anything past the tile) is padding and re-reads the
+  // row's first chunk.  V (bf16): chunk I*64 + L is row r, position p, and
+  // carries global chunk p ^ swz_v(r).  Keys past the end re-read the last key
+  // (always masked by causality).
+  Vec16<T> vreg[TL::VREG];
+  auto issue_tile = [&](int it, int buf) {
+    const int j0 = (it < ta ? it : tb + (it - ta)) * BN;
+    for (int inst = wave; inst < TL::K_DMA; inst += NW) {
+      const int m = inst * 64 + lane;
+      const int r = min(m / (CPR + 1), BN - 1);
+      const int c = m % (CPR + 1);
+      const int64_t j = min(int64_t(j0 + r), n - 1);
+      dma16(kg + j * kv_row_bytes + (c < CPR ? c : 0) * 16, &sK[buf][inst * 1024]);
+    }
+    if constexpr (TL::kTr) {
+#pragma unroll
+      for (int i = 0; i < TL::V_DMA_PER_WAVE; ++i) {
+        const int inst = wave * TL::V_DMA_PER_WAVE + i;
+        const int m = inst * 64 + lane;
+        const int r = m / CPR, p = m % CPR;
+        const int64_t j = min(int64_t(j0 + r), n - 1);
+        dma16(vg + j * kv_row_bytes + (p ^ TL::swz_v(r)) * 16, &sV[buf][inst * 1024]);
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < TL::VREG; ++i) {
+        const int idx = threadIdx.x + i * NW * 64;
+        const int r = idx / CPR, cc = idx % CPR;
+        const int64_t j = min(int64_t(j0 + r), n - 1);
+        vreg[i] = load16(reinterpret_cast<const T*>(vg + j * kv_row_bytes) + cc * EPL);
+      }
+    }
+  };
+  // fp32: V^T[d][key] is written from the staged registers.
+  auto store_vt = [&](int buf) {
+    if constexpr (!TL::kTr) {
+      T* vt = reinterpret_cast<T*>(&sV[buf][0]);
+#pragma unroll
+      for (int i = 0; i < TL::VREG; ++i) {
+        const int idx = threadIdx.x + i * NW * 64;
+        const int r = idx / CPR, cc = idx % CPR;
+#pragma unroll
+        for (int e = 0; e < EPL; ++e) vt[(cc * EPL + e) * TL::VT_LD + r] = vreg[i].v[e];
+      }
+    }
+  };
+
+  // Per-lane byte offsets of the MFMA operand reads (tile independent).
+  // K operand: row lrow (+ 32 * sub), head-dim elements [kk*K + half*K/2, +K/2).
+  const int k_lane = lrow * RBP + half * (M::K / 2) * int(sizeof(T));
+  // Transposing V read: lane 16G + 4e + a points at row (G/2)*4 + e (+ kb0),
+  // bf16 column 32*dt + 16*(G%2) + 4a.
+  int v_off[D / 32];
+  if constexpr (TL::kTr) {
+    const int vr = (lane >> 5) * 4 + ((lane & 15) >> 2);    // row mod 8
+    const int a4 = lane & 3;
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) {
+      const int q = dt * 4 + ((lane >> 4) & 1) * 2 + (a4 >> 1);
+      v_off[dt] = vr * RB + ((q ^ TL::swz_v(vr)) * 16) + (a4 & 1) * 8;
+    }
+  } else {
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) v_off[dt] = (dt * 32 + lrow) * TL::VT_LD * int(sizeof(T));
+  }
+
   f32x16 oacc[D / 32];
 #pragma unroll
   for (int dt = 0; dt < D / 32; ++dt) oacc[dt] = f32x16{};
   float m_run = kNegBig, l_run = 0.0f;
   const int my_row = iw0 + lrow;
 
+  if (ntiles > 0) issue_tile(0, 0);
   for (int it = 0; it < ntiles; ++it) {
-    const int t = it < ta ? it : tb + (it - ta);
-    const int j0 = t * BN;
-
-    // Stage K (row-major) and V (transposed) of keys j0 .. j0+BN-1.
-    __syncthreads();
-    for (int idx = threadIdx.x; idx < BN * CPR; idx += blockDim.x) {
-      const int r = idx / CPR, cc = idx % CPR;
-      const int j = j0 + r;
-      Vec16<T> kx, vx;
-      if (j < n) {
-        kx = load16(kg + int64_t(j) * kv_row_stride + cc * EPL);
-        vx = load16(vg + int64_t(j) * kv_row_stride + cc * EPL);
-      } else {
-        kx = zero16<T>();
-        vx = zero16<T>();
-      }
-      store16(sK + r * LDK + cc * EPL, kx);
-#pragma unroll
-      for (int e = 0; e < EPL; ++e) sV[(cc * EPL + e) * LDV + r] = vx.v[e];
-    }
-    __syncthreads();
+    const int buf = it & 1;
+    const int j0 = (it < ta ? it : tb + (it - ta)) * BN;
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this thread's loads of tile `it` landed
+    store_vt(buf);
+    __syncthreads();                      // ... for every thread; buffer buf^1 is free again
+    if (it + 1 < ntiles) issue_tile(it + 1, buf ^ 1);
 
     if (!wave_active) continue;
     // Does any (row, key) pair of this wave fall inside the mask?
@@ -159,53 +265,70 @@ __global__ void __launch_bounds__(256) prefill_kernel(PrefillArgs a) {
                          ((j0 + BN <= s) || ((iw1 - 1) - j0 < w));
 
     // S^T = K Q^T for two 32-key sub-tiles.
+    const char* kb = &sK[buf][0];
     f32x16 sacc[2];
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
       sacc[sub] = f32x16{};
-      const T* krow = sK + (sub * 32 + lrow) * LDK;
 #pragma unroll
-      for (int kk = 0; kk < KS; ++kk) sacc[sub] = M::mma(load_frag(krow, kk, half), qf[kk], sacc[sub]);
-    }
-
-    // Scale into base 2, mask, tile row max.
-    float tmax = -INFINITY;
-#pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float x = sacc[sub][r] * a.scale_log2;
-        if (!all_vis) {
-          const int j = j0 + sub * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
-          const bool vis = (j <= my_row) && (j < s || my_row - j < w) && (my_row < i1);
-          x = vis ? x : -INFINITY;
-        }
-        sacc[sub][r] = x;
-        tmax = fmaxf(tmax, x);
+      for (int kk = 0; kk < KS; ++kk) {
+        const typename M::frag kf = *reinterpret_cast<const typename M::frag*>(
+            kb + k_lane + sub * 32 * RBP + kk * M::K * int(sizeof(T)));
+        sacc[sub] = M::mma(kf, qf[kk], sacc[sub]);
       }
     }
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-    const float m_new = fmaxf(m_run, tmax);
-    const float alpha = fast_exp2(m_run - m_new);
-    m_run = m_new;
+
+    // Mask (edge tiles only; branch-free selects) and the tile's raw row maximum.
+    if (!all_vis) {
+      const int jl = j0 + half * 4;                 // key of register 0 of this lane
+      const int hi = my_row < i1 ? my_row - jl : -1;  // causal: key offset <= hi
+      const int band = my_row - w + 1 - jl;           // band: key offset >= band
+      const int sink = s - jl;                        // sink: key offset < sink
+#pragma unroll
+      for (int sub = 0; sub < 2; ++sub) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int dj = sub * 32 + (r >> 2) * 8 + (r & 3);
+          const bool vis = (dj <= hi) & ((dj < sink) | (dj >= band));
+          sacc[sub][r] = vis ? sacc[sub][r] : -INFINITY;
+        }
+      }
+    }
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, sacc[sub][r]);
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64)) * c2;
+    // Raise the exponent offset only when some row of the wave needs it.
+    if (__any(tmax > m_run + kRescaleSlack)) {
+      const float m_new = fmaxf(m_run, tmax);
+      const float alpha = fast_exp2(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
+#pragma unroll
+      for (int dt = 0; dt < D / 32; ++dt) oacc[dt] *= alpha;
+    }
 
     float psum = 0.0f;
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const float p = fast_exp2(sacc[sub][r] - m_new);
+        // bf16: one FMA per score.  fp32: separately rounded product, so a
+        // row's maximal score gives exactly 2^0 (w = 1 returns v bit-exactly).
+        const float p = sizeof(T) == 2 ? fast_exp2(__builtin_fmaf(sacc[sub][r], c2, -m_run))
+                                       : fast_exp2(mul_then_sub(sacc[sub][r], c2, m_run));
         sacc[sub][r] = p;
         psum += p;
       }
     }
     psum += __shfl_xor(psum, 32, 64);
-    l_run = l_run * alpha + psum;
-#pragma unroll
-    for (int dt = 0; dt < D / 32; ++dt) oacc[dt] *= alpha;
+    l_run += psum;
 
     // O^T += V^T P^T.
-    if constexpr (sizeof(T) == 2) {
+    const char* vb = &sV[buf][0];
+    if constexpr (TL::kTr) {
       bf16x8 pf[2][2];
 #pragma unroll
       for (int sub = 0; sub < 2; ++sub)
@@ -215,14 +338,13 @@ __global__ void __launch_bounds__(256) prefill_kernel(PrefillArgs a) {
           for (int e = 0; e < 8; ++e) pf[sub][c][e] = static_cast<bf16>(sacc[sub][8 * c + e]);
 #pragma unroll
       for (int dt = 0; dt < D / 32; ++dt) {
-        const T* vrow = sV + (dt * 32 + lrow) * LDV;
 #pragma unroll
         for (int sub = 0; sub < 2; ++sub) {
 #pragma unroll
           for (int c = 0; c < 2; ++c) {
-            const int kb = sub * 32 + 16 * c + half * 4;
-            const bf16x4 lo4 = *reinterpret_cast<const bf16x4*>(vrow + kb);
-            const bf16x4 hi4 = *reinterpret_cast<const bf16x4*>(vrow + kb + 8);
+            const int kb0 = sub * 32 + 16 * c;
+            const bf16x4 lo4 = read_tr(reinterpret_cast<const bf16*>(vb + kb0 * RB + v_off[dt]));
+            const bf16x4 hi4 = read_tr(reinterpret_cast<const bf16*>(vb + (kb0 + 8) * RB + v_off[dt]));
             const bf16x8 vf = __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7);
             oacc[dt] = M::mma(vf, pf[sub][c], oacc[dt]);
           }
@@ -231,13 +353,13 @@ __global__ void __launch_bounds__(256) prefill_kernel(PrefillArgs a) {
     } else {
 #pragma unroll
       for (int dt = 0; dt < D / 32; ++dt) {
-        const T* vrow = sV + (dt * 32 + lrow) * LDV;
+        const T* vt = reinterpret_cast<const T*>(vb + v_off[dt]);
 #pragma unroll
         for (int sub = 0; sub < 2; ++sub) {
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int key = sub * 32 + (r >> 2) * 8 + half * 4 + (r & 3);
-            oacc[dt] = M::mma(vrow[key], sacc[sub][r], oacc[dt]);
+            oacc[dt] = M::mma(vt[key], sacc[sub][r], oacc[dt]);
           }
         }
       }

@@ -163,3 +163,12 @@ def test_binding_fails_loudly_without_library(tmp_path):
             M.load_library(str(tmp_path / "missing.so"))
     finally:
         M._lib = saved
+
+
+def test_library_resolves_all_of_its_own_symbols():
+    # Every kernel stub and entry point must be defined inside libmoa.so itself.
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--undefined-only", M.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    own = [line for line in out.splitlines() if "moa" in line]
+    assert own == [], own
