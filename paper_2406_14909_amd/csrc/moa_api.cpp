@@ -113,11 +113,10 @@ moa_status_t moa_plan(const moa_desc_t* desc, const double* alpha, const double*
     p->capacity[h] = static_cast<int32_t>(w + d.num_sink);
     p->offset[h + 1] = p->offset[h] + p->capacity[h];
   }
-  p->head_order.resize(d.num_q_heads);
-  std::iota(p->head_order.begin(), p->head_order.end(), 0);
-  std::stable_sort(p->head_order.begin(), p->head_order.end(), [&](int16_t a, int16_t b) {
-    return p->window[a / group] > p->window[b / group];
-  });
+  p->kv_order.resize(hkv);
+  std::iota(p->kv_order.begin(), p->kv_order.end(), 0);
+  std::stable_sort(p->kv_order.begin(), p->kv_order.end(),
+                   [&](int16_t a, int16_t b) { return p->window[a] > p->window[b]; });
   *out = p;
   return ok();
 }
@@ -150,7 +149,11 @@ moa_status_t moa_prefill(const moa_plan_t* plan, const void* q, const void* k, c
   if (overlaps(o, qbytes, q, qbytes) || overlaps(o, qbytes, k, kbytes) || overlaps(o, qbytes, v, kbytes))
     return fail(MOA_ERR_INVALID_ARG, "moa_prefill: output overlaps an input");
   const int64_t tiles = (n_tokens + kPrefillRows - 1) / kPrefillRows;
-  if (tiles * batch * d.num_q_heads >= (int64_t(1) << 31))
+  const int64_t qchunk = std::min<int64_t>(kPrefillChunk, tiles);
+  const int64_t n_chunks = (tiles + qchunk - 1) / qchunk;
+  const int64_t n_units = int64_t(d.num_kv_heads) * batch * n_chunks;
+  const int64_t blocks = (n_units + kNumXcd - 1) / kNumXcd * kNumXcd * plan->group * qchunk;
+  if (blocks >= (int64_t(1) << 31))
     return fail(MOA_ERR_UNSUPPORTED, "moa_prefill: too many work-groups for one launch");
 
   PrefillArgs a;
@@ -163,9 +166,14 @@ moa_status_t moa_prefill(const moa_plan_t* plan, const void* q, const void* k, c
   a.group = plan->group;
   a.num_sink = d.num_sink;
   a.n_qtiles = static_cast<int32_t>(tiles);
+  a.qchunk = static_cast<int32_t>(qchunk);
+  a.n_chunks = static_cast<int32_t>(n_chunks);
+  a.n_units = static_cast<int32_t>(n_units);
   a.scale_log2 = plan->scale * 1.4426950408889634f;
-  for (int h = 0; h < d.num_kv_heads; ++h) a.window[h] = plan->window[h];
-  for (int h = 0; h < d.num_q_heads; ++h) a.head_order[h] = plan->head_order[h];
+  for (int h = 0; h < d.num_kv_heads; ++h) {
+    a.window[h] = plan->window[h];
+    a.kv_order[h] = plan->kv_order[h];
+  }
   const int err = launch_prefill(a, d.dtype, d.head_dim, hip_stream);
   if (err) return fail(MOA_ERR_HIP, "moa_prefill: kernel launch failed (hipError " + std::to_string(err) + ")");
   return ok();

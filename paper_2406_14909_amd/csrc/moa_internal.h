@@ -19,7 +19,7 @@ struct moa_plan_s {
   std::vector<int32_t> window;     // [H_kv]
   std::vector<int32_t> capacity;   // [H_kv]
   std::vector<int64_t> offset;     // [H_kv + 1]
-  std::vector<int16_t> head_order; // [H_q] query heads, widest window first
+  std::vector<int16_t> kv_order;   // [H_kv] KV heads, widest window first
 };
 
 namespace moa {
@@ -51,9 +51,12 @@ struct PrefillArgs {
   int32_t group;
   int32_t num_sink;
   int32_t n_qtiles;          // ceil(n / query rows per block)
+  int32_t qchunk;            // query tiles per dispatch unit
+  int32_t n_chunks;          // ceil(n_qtiles / qchunk)
+  int32_t n_units;           // hkv * batch * n_chunks
   float scale_log2;          // softmax scale * log2(e)
   int32_t window[MOA_MAX_KV_HEADS];
-  int16_t head_order[MOA_MAX_Q_HEADS];
+  int16_t kv_order[MOA_MAX_KV_HEADS];
 };
 
 struct AppendArgs {
@@ -98,6 +101,8 @@ int launch_kv_append(const AppendArgs& a, int dtype, int head_dim, void* stream)
 int launch_decode(const DecodeArgs& a, int dtype, int head_dim, int group, void* stream);
 
 constexpr int kPrefillRows = 128;   // query rows per prefill work-group
+constexpr int kPrefillChunk = 16;   // query tiles per prefill dispatch unit
+constexpr int kNumXcd = 8;          // accelerator dies; work-groups go round-robin over them
 constexpr int kDecodeChunk = 512;   // cache slots per decode work item
 
 }  // namespace moa

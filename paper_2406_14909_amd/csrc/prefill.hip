@@ -21,7 +21,8 @@
 // The key order inside each 16-key MFMA step is permuted identically on both
 // operands, which leaves the sum unchanged.
 // Softmax is online in base 2 with the scale folded into one FMA per score
-// (bf16 instantiation).
+// (bf16 instantiation); the row sum is accumulated over the bf16-rounded
+// probabilities that the PV product uses.
 // The running maximum used as the exponent offset is raised only when some
 // row of the wave would otherwise see exponents above 2^8 (a wave-uniform
 // test), so most tiles skip rescaling the output accumulator; the final
@@ -82,6 +83,18 @@ __device__ __forceinline__ bf16x4 read_tr(const bf16* p) {
 #endif
 }
 
+// acc + a + b with a, b in bf16 (v_dot2_f32_bf16 against (1, 1)).
+__device__ __forceinline__ float dot2_ones(bf16 a, bf16 b, float acc) {
+  typedef bf16 bf16x2 __attribute__((ext_vector_type(2)));
+#if defined(__HIP_DEVICE_COMPILE__)
+  const bf16x2 ab = {a, b};
+  const bf16x2 ones = {bf16(1.0f), bf16(1.0f)};
+  return __builtin_amdgcn_fdot2_f32_bf16(ab, ones, acc, false);
+#else
+  return acc + float(a) + float(b);
+#endif
+}
+
 // x * y - z with the product rounded on its own (never fused).
 __device__ __forceinline__ float mul_then_sub(float x, float y, float z) {
 #pragma clang fp contract(off)
@@ -123,18 +136,32 @@ __global__ void __launch_bounds__(NW * 64, 2) prefill_kernel(PrefillArgs a) {
   __shared__ __attribute__((aligned(1024))) char sV[2][TL::V_BYTES];
 
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave-uniform (scalar)
   const int lrow = lane & 31;
   const int half = lane >> 5;
 
-  // Work item: query tiles from last to first (heaviest first), then query
-  // heads in decreasing window order, then sequences.
-  const int per_tile = a.batch * a.hq;
-  const int qt = a.n_qtiles - 1 - static_cast<int>(blockIdx.x / per_tile);
-  const int rem = static_cast<int>(blockIdx.x % per_tile);
-  const int h = a.head_order[rem / a.batch];
-  const int b = rem % a.batch;
-  const int g = h / a.group;
+  // Work item.  A dispatch unit is (KV head, sequence, qchunk consecutive
+  // query tiles) with all `group` query heads of that KV head, so its work-
+  // groups share K/V bands.  Units are ordered heaviest first (latest query
+  // chunks first, then widest window) and dealt to the accelerator dies in
+  // rounds of kNumXcd, alternating direction each round: work-group i runs on
+  // die i % kNumXcd, which walks its units in order, so the work-groups
+  // resident on one die at a time share that die's L2, and every die gets a
+  // similar mix of heavy and light units.
+  const int xcd = static_cast<int>(blockIdx.x % kNumXcd);
+  const int local = static_cast<int>(blockIdx.x / kNumXcd);
+  const int per_unit = a.group * a.qchunk;
+  const int round = local / per_unit;
+  const int unit = round * kNumXcd + ((round & 1) ? kNumXcd - 1 - xcd : xcd);
+  if (unit >= a.n_units) return;                   // padding unit
+  const int within = local % per_unit;
+  const int hb = a.hkv * a.batch;
+  const int cd = unit / hb;                        // chunk rank, heaviest first
+  const int g = a.kv_order[(unit % hb) / a.batch];
+  const int b = unit % a.batch;
+  const int qt = (a.n_chunks - 1 - cd) * a.qchunk + (a.qchunk - 1 - within / a.group);
+  if (qt >= a.n_qtiles) return;                     // past the last query tile
+  const int h = g * a.group + within % a.group;
   const int64_t n = a.n;
   const int w = a.window[g];
   const int s = a.num_sink;
@@ -179,26 +206,64 @@ __global__ void __launch_bounds__(NW * 64, 2) prefill_kernel(PrefillArgs a) {
   // row's first chunk.  V (bf16): chunk I*64 + L is row r, position p, and
   // carries global chunk p ^ swz_v(r).  Keys past the end re-read the last key
   // (always masked by causality).
+  // Per-lane byte offsets of the DMA sources relative to the tile's first key
+  // row (tile independent); rows are kept for the clamped path of a tile that
+  // runs past the last key.
+  constexpr int KI = (TL::K_DMA + NW - 1) / NW;      // K DMA instructions per wave (some idle)
+  uint32_t k_src[KI], v_src[TL::kTr ? TL::V_DMA_PER_WAVE : 1];
+  int k_r[KI], v_r[TL::kTr ? TL::V_DMA_PER_WAVE : 1];
+#pragma unroll
+  for (int i = 0; i < KI; ++i) {
+    const int m = (wave + i * NW) * 64 + lane;
+    const int r = min(m / (CPR + 1), BN - 1);
+    const int c = m % (CPR + 1);
+    k_r[i] = r;
+    k_src[i] = uint32_t(r) * uint32_t(kv_row_bytes) + uint32_t(c < CPR ? c : 0) * 16u;
+  }
+  if constexpr (TL::kTr) {
+#pragma unroll
+    for (int i = 0; i < TL::V_DMA_PER_WAVE; ++i) {
+      const int m = (wave * TL::V_DMA_PER_WAVE + i) * 64 + lane;
+      const int r = m / CPR, p = m % CPR;
+      v_r[i] = r;
+      v_src[i] = uint32_t(r) * uint32_t(kv_row_bytes) + uint32_t(p ^ TL::swz_v(r)) * 16u;
+    }
+  }
   Vec16<T> vreg[TL::VREG];
   auto issue_tile = [&](int it, int buf) {
     const int j0 = (it < ta ? it : tb + (it - ta)) * BN;
-    for (int inst = wave; inst < TL::K_DMA; inst += NW) {
-      const int m = inst * 64 + lane;
-      const int r = min(m / (CPR + 1), BN - 1);
-      const int c = m % (CPR + 1);
-      const int64_t j = min(int64_t(j0 + r), n - 1);
-      dma16(kg + j * kv_row_bytes + (c < CPR ? c : 0) * 16, &sK[buf][inst * 1024]);
-    }
-    if constexpr (TL::kTr) {
+    const char* kt = kg + int64_t(j0) * kv_row_bytes;
+    const char* vt = vg + int64_t(j0) * kv_row_bytes;
+    if (int64_t(j0) + BN <= n) {                    // common case: every row is a real key
 #pragma unroll
-      for (int i = 0; i < TL::V_DMA_PER_WAVE; ++i) {
-        const int inst = wave * TL::V_DMA_PER_WAVE + i;
-        const int m = inst * 64 + lane;
-        const int r = m / CPR, p = m % CPR;
-        const int64_t j = min(int64_t(j0 + r), n - 1);
-        dma16(vg + j * kv_row_bytes + (p ^ TL::swz_v(r)) * 16, &sV[buf][inst * 1024]);
+      for (int i = 0; i < KI; ++i) {
+        const int inst = wave + i * NW;
+        if (inst < TL::K_DMA) dma16(kt + k_src[i], &sK[buf][inst * 1024]);
       }
-    } else {
+      if constexpr (TL::kTr) {
+#pragma unroll
+        for (int i = 0; i < TL::V_DMA_PER_WAVE; ++i) {
+          const int inst = wave * TL::V_DMA_PER_WAVE + i;
+          dma16(vt + v_src[i], &sV[buf][inst * 1024]);
+        }
+      }
+    } else {                                         // last tile: rows past the end re-read key n-1
+#pragma unroll
+      for (int i = 0; i < KI; ++i) {
+        const int inst = wave + i * NW;
+        const int64_t extra = (min(int64_t(j0 + k_r[i]), n - 1) - (j0 + k_r[i])) * kv_row_bytes;
+        if (inst < TL::K_DMA) dma16(kt + k_src[i] + extra, &sK[buf][inst * 1024]);
+      }
+      if constexpr (TL::kTr) {
+#pragma unroll
+        for (int i = 0; i < TL::V_DMA_PER_WAVE; ++i) {
+          const int inst = wave * TL::V_DMA_PER_WAVE + i;
+          const int64_t extra = (min(int64_t(j0 + v_r[i]), n - 1) - (j0 + v_r[i])) * kv_row_bytes;
+          dma16(vt + v_src[i] + extra, &sV[buf][inst * 1024]);
+        }
+      }
+    }
+    if constexpr (!TL::kTr) {
 #pragma unroll
       for (int i = 0; i < TL::VREG; ++i) {
         const int idx = threadIdx.x + i * NW * 64;
@@ -265,17 +330,24 @@ __global__ void __launch_bounds__(NW * 64, 2) prefill_kernel(PrefillArgs a) {
                          ((j0 + BN <= s) || ((iw1 - 1) - j0 < w));
 
     // S^T = K Q^T for two 32-key sub-tiles.
-    const char* kb = &sK[buf][0];
-    f32x16 sacc[2];
+    // Fragments of step kk+1 are read while the MFMAs of step kk run; the two
+    // 32-key chains alternate so consecutive MFMAs are independent.
+    const char* kb = &sK[buf][k_lane];
+    auto kfrag = [&](int kk, int sub) {
+      return *reinterpret_cast<const typename M::frag*>(kb + sub * 32 * RBP + kk * M::K * int(sizeof(T)));
+    };
+    f32x16 sacc[2] = {f32x16{}, f32x16{}};
+    typename M::frag kf[2][2];
+    kf[0][0] = kfrag(0, 0);
+    kf[0][1] = kfrag(0, 1);
 #pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {
-      sacc[sub] = f32x16{};
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk) {
-        const typename M::frag kf = *reinterpret_cast<const typename M::frag*>(
-            kb + k_lane + sub * 32 * RBP + kk * M::K * int(sizeof(T)));
-        sacc[sub] = M::mma(kf, qf[kk], sacc[sub]);
+    for (int kk = 0; kk < KS; ++kk) {
+      if (kk + 1 < KS) {
+        kf[(kk + 1) & 1][0] = kfrag(kk + 1, 0);
+        kf[(kk + 1) & 1][1] = kfrag(kk + 1, 1);
       }
+      sacc[0] = M::mma(kf[kk & 1][0], qf[kk], sacc[0]);
+      sacc[1] = M::mma(kf[kk & 1][1], qf[kk], sacc[1]);
     }
 
     // Mask (edge tiles only; branch-free selects) and the tile's raw row maximum.
@@ -310,47 +382,62 @@ __global__ void __launch_bounds__(NW * 64, 2) prefill_kernel(PrefillArgs a) {
       for (int dt = 0; dt < D / 32; ++dt) oacc[dt] *= alpha;
     }
 
-    float psum = 0.0f;
-#pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        // bf16: one FMA per score.  fp32: separately rounded product, so a
-        // row's maximal score gives exactly 2^0 (w = 1 returns v bit-exactly).
-        const float p = sizeof(T) == 2 ? fast_exp2(__builtin_fmaf(sacc[sub][r], c2, -m_run))
-                                       : fast_exp2(mul_then_sub(sacc[sub][r], c2, m_run));
-        sacc[sub][r] = p;
-        psum += p;
-      }
-    }
-    psum += __shfl_xor(psum, 32, 64);
-    l_run += psum;
-
-    // O^T += V^T P^T.
     const char* vb = &sV[buf][0];
     if constexpr (TL::kTr) {
+      // P in bf16; the row sum is taken over the same rounded weights that
+      // enter the PV product (dot2 with (1, 1)).
       bf16x8 pf[2][2];
+      float psum = 0.0f;
 #pragma unroll
-      for (int sub = 0; sub < 2; ++sub)
+      for (int sub = 0; sub < 2; ++sub) {
 #pragma unroll
-        for (int c = 0; c < 2; ++c)
+        for (int c = 0; c < 2; ++c) {
 #pragma unroll
-          for (int e = 0; e < 8; ++e) pf[sub][c][e] = static_cast<bf16>(sacc[sub][8 * c + e]);
+          for (int e = 0; e < 8; ++e)
+            pf[sub][c][e] = static_cast<bf16>(fast_exp2(__builtin_fmaf(sacc[sub][8 * c + e], c2, -m_run)));
 #pragma unroll
-      for (int dt = 0; dt < D / 32; ++dt) {
-#pragma unroll
-        for (int sub = 0; sub < 2; ++sub) {
-#pragma unroll
-          for (int c = 0; c < 2; ++c) {
-            const int kb0 = sub * 32 + 16 * c;
-            const bf16x4 lo4 = read_tr(reinterpret_cast<const bf16*>(vb + kb0 * RB + v_off[dt]));
-            const bf16x4 hi4 = read_tr(reinterpret_cast<const bf16*>(vb + (kb0 + 8) * RB + v_off[dt]));
-            const bf16x8 vf = __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7);
-            oacc[dt] = M::mma(vf, pf[sub][c], oacc[dt]);
-          }
+          for (int e = 0; e < 8; e += 2) psum = dot2_ones(pf[sub][c][e], pf[sub][c][e + 1], psum);
         }
       }
+      psum += __shfl_xor(psum, 32, 64);
+      l_run += psum;
+
+      // O^T += V^T P^T: for each 16-key step the four d-tile accumulators are
+      // independent; the V^T fragments of the next step are read meanwhile.
+      auto vfrag = [&](int step, int dt) {
+        const int kb0 = (step >> 1) * 32 + 16 * (step & 1);
+        const bf16x4 lo4 = read_tr(reinterpret_cast<const bf16*>(vb + kb0 * RB + v_off[dt]));
+        const bf16x4 hi4 = read_tr(reinterpret_cast<const bf16*>(vb + (kb0 + 8) * RB + v_off[dt]));
+        return __builtin_shufflevector(lo4, hi4, 0, 1, 2, 3, 4, 5, 6, 7);
+      };
+      bf16x8 vf[2][D / 32];
+#pragma unroll
+      for (int dt = 0; dt < D / 32; ++dt) vf[0][dt] = vfrag(0, dt);
+#pragma unroll
+      for (int step = 0; step < 4; ++step) {
+        if (step + 1 < 4) {
+#pragma unroll
+          for (int dt = 0; dt < D / 32; ++dt) vf[(step + 1) & 1][dt] = vfrag(step + 1, dt);
+        }
+#pragma unroll
+        for (int dt = 0; dt < D / 32; ++dt)
+          oacc[dt] = M::mma(vf[step & 1][dt], pf[step >> 1][step & 1], oacc[dt]);
+      }
     } else {
+      float psum = 0.0f;
+#pragma unroll
+      for (int sub = 0; sub < 2; ++sub) {
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          // separately rounded product: a row's maximal score gives exactly
+          // 2^0, so w = 1 returns v bit-exactly in fp32
+          const float p = fast_exp2(mul_then_sub(sacc[sub][r], c2, m_run));
+          sacc[sub][r] = p;
+          psum += p;
+        }
+      }
+      psum += __shfl_xor(psum, 32, 64);
+      l_run += psum;
 #pragma unroll
       for (int dt = 0; dt < D / 32; ++dt) {
         const T* vt = reinterpret_cast<const T*>(vb + v_off[dt]);
@@ -391,7 +478,7 @@ __global__ void __launch_bounds__(NW * 64, 2) prefill_kernel(PrefillArgs a) {
 
 template <typename T, int D>
 int launch_t(const PrefillArgs& a, void* stream) {
-  const int64_t blocks = int64_t(a.n_qtiles) * a.batch * a.hq;
+  const int64_t blocks = int64_t((a.n_units + kNumXcd - 1) / kNumXcd) * kNumXcd * a.group * a.qchunk;
   PrefillArgs copy = a;
   void* args[] = {&copy};
   return static_cast<int>(hipLaunchKernel(reinterpret_cast<const void*>(&prefill_kernel<T, D>),
