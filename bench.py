@@ -30,6 +30,36 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+ROOT = os.path.dirname(os.path.abspath(__file__))
+
+
+def measured_traffic(profile: str):
+    """HBM bytes per launch recorded in profiles/<profile> by rocprofv3
+    FETCH_SIZE / WRITE_SIZE passes (scaled by the copy-kernel calibration), or
+    None when the kernel sources changed since the counters were taken."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", profile)
+    if not os.path.exists(path):
+        return None
+    fields = {}
+    for line in open(path):
+        key, sep, val = line.partition(":")
+        if sep and key.strip() in ("traffic_bytes_per_launch", "source_files", "source_sha256"):
+            fields[key.strip()] = val.strip()
+    if len(fields) != 3:
+        return None
+    h = hashlib.sha256()
+    for f in fields["source_files"].split():
+        src = os.path.join(ROOT, "paper_2406_14909_amd", "csrc", f)
+        if not os.path.exists(src):
+            return None
+        h.update(open(src, "rb").read())
+    if h.hexdigest() != fields["source_sha256"]:
+        return None
+    return int(float(fields["traffic_bytes_per_launch"]))
+
+
 def visible_pairs(n: int, w: int, s: int) -> int:
     """sum_{i<n} |{j <= i : j < s or i - j < w}| (closed form per row)."""
     total = 0
@@ -55,6 +85,9 @@ def main() -> int:
     ap.add_argument("--workload", default="vicuna7b-decode-b32-ctx8192")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds per oracle leg")
+    ap.add_argument("--profile-kernel", choices=["decode", "prefill", "append", "copy"], default=None,
+                    help="launch only this kernel --reps times on the bench workload (hardware-counter runs)")
+    ap.add_argument("--reps", type=int, default=3)
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -104,6 +137,10 @@ def main() -> int:
         fills = sum(min(t + 1, c) for c in caps)
         dec_bytes.append(B * fills * D * 2 * esz + 2 * B * Hq * D * esz)
     dec_bytes_total = float(sum(dec_bytes))
+
+    if args.profile_kernel:
+        return profile_kernel(args, M, plan, q_pre, k_pre, v_pre, o_pre, q_dec, k_dec, v_dec, o_dec,
+                              kc, vc, pos, ws, N, prefill_flops, dec_bytes[0])
 
     stream = torch.cuda.current_stream()
     n_ev = steps_dec + 1
@@ -185,7 +222,8 @@ def main() -> int:
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
-            "traffic": None,
+            "traffic": measured_traffic("hbm_traffic__decode_kernel__vicuna7b-decode-b32-ctx8192.md"),
+            "traffic_kernel": "decode_kernel<bf16,128,1> (bytes per launch)",
             "bytes_per_launch": round(dec_bytes_total / steps_dec),
         },
         "roofline_prefill": {
@@ -195,7 +233,7 @@ def main() -> int:
             "peak": BF16_MFMA_PEAK_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(pre_tflops / BF16_MFMA_PEAK_TFLOPS, 4),
-            "traffic": None,
+            "traffic": measured_traffic("hbm_traffic__prefill_kernel__vicuna7b-b32-n8192.md"),
             "flops_per_launch": prefill_flops,
         },
     }
@@ -204,6 +242,46 @@ def main() -> int:
         result["cpu_baseline"] = cpu_baseline(wl, plan, q_pre, k_pre, v_pre, q_dec, k_dec, v_dec,
                                               steps_dec, args.cpu_budget)
     print(json.dumps(result), flush=True)
+    return 0
+
+
+def profile_kernel(args, M, plan, q_pre, k_pre, v_pre, o_pre, q_dec, k_dec, v_dec, o_dec, kc, vc, pos,
+                   ws, N, prefill_flops, dec_bytes):
+    """Launches one kernel of the workload --reps times (for rocprofv3 --pmc runs).
+
+    decode: moa_decode at position N over the caches filled from the prompt;
+    prefill: moa_prefill of the prompt; append: one-token moa_kv_append;
+    copy: a plain 1 GiB device copy (calibrates FETCH_SIZE / WRITE_SIZE).
+    Prints one JSON line with the algorithmic work per launch.
+    """
+    import torch
+
+    info = {"kernel": args.profile_kernel, "reps": args.reps}
+    if args.profile_kernel in ("decode", "append"):
+        M.moa_kv_append(plan, kc, vc, pos, k_pre, v_pre, 0)
+        M.moa_kv_append(plan, kc, vc, pos, k_dec[0], v_dec[0], N)
+    torch.cuda.synchronize()
+    for _ in range(args.reps):
+        if args.profile_kernel == "decode":
+            M.moa_decode(plan, q_dec[0], kc, vc, N, ws, o_dec)
+        elif args.profile_kernel == "prefill":
+            M.moa_prefill(plan, q_pre, k_pre, v_pre, o_pre)
+        elif args.profile_kernel == "append":
+            M.moa_kv_append(plan, kc, vc, pos, k_dec[0], v_dec[0], N)
+    if args.profile_kernel == "copy":
+        nbytes = 1 << 30
+        src = torch.ones(nbytes // 2, dtype=torch.bfloat16, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(args.reps):
+            dst.copy_(src)
+        info["bytes_read_per_launch"] = nbytes
+        info["bytes_written_per_launch"] = nbytes
+    elif args.profile_kernel == "decode":
+        info["algorithmic_bytes_per_launch"] = dec_bytes
+    elif args.profile_kernel == "prefill":
+        info["algorithmic_flops_per_launch"] = prefill_flops
+    torch.cuda.synchronize()
+    print(json.dumps(info), flush=True)
     return 0
 
 

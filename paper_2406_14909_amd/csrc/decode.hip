@@ -174,27 +174,60 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
 }
 
 // Merges the split-K partials of every (sequence, KV head) with more than one
-// chunk: o = sum_c 2^(m_c - M) acc_c / sum_c 2^(m_c - M) l_c, M = max_c m_c.
+// chunk: o = sum_c w_c acc_c with w_c = 2^(m_c - M) / sum_c' 2^(m_c' - M) l_c',
+// M = max_c m_c.  The per-chunk (m, l) are staged in LDS once (the plan keeps
+// every cache within kMaxMergeChunks chunks); the weighted sum over chunks
+// then issues independent, coalesced loads per output.
+
 template <typename T, int D, int G>
 __global__ void __launch_bounds__(256) decode_combine_kernel(DecodeArgs a) {
+  __shared__ float s_w[G][kMaxMergeChunks];
+  __shared__ float s_inv[G];
   const int b = blockIdx.x / a.hkv;
   const int g = blockIdx.x - b * a.hkv;
   const int nchunk = a.item_start[g + 1] - a.item_start[g];
   if (nchunk == 1) return;
   const int64_t first = int64_t(b) * a.items_per_seq + a.item_start[g];
+  // 1) raw running maxima into LDS
+  for (int t = threadIdx.x; t < G * nchunk; t += blockDim.x) {
+    const int h = t / nchunk, c = t % nchunk;
+    s_w[h][c] = a.part[((first + c) * G + h) * (D + 2) + D];
+  }
+  __syncthreads();
+  // 2) one wave per query head: weights 2^(m_c - M) and 1 / sum_c 2^(m_c - M) l_c
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int h = wave; h < G; h += blockDim.x / 64) {
+    float mx = kNegBig;
+    for (int c = lane; c < nchunk; c += 64) mx = fmaxf(mx, s_w[h][c]);
+#pragma unroll
+    for (int off = 32; off >= 1; off /= 2) mx = fmaxf(mx, __shfl_xor(mx, off, 64));
+    float lsum = 0.0f;
+    for (int c = lane; c < nchunk; c += 64) {
+      const float f = fast_exp2(s_w[h][c] - mx);
+      s_w[h][c] = f;
+      lsum += f * a.part[((first + c) * G + h) * (D + 2) + D + 1];
+    }
+#pragma unroll
+    for (int off = 32; off >= 1; off /= 2) lsum += __shfl_xor(lsum, off, 64);
+    if (lane == 0) s_inv[h] = 1.0f / lsum;
+  }
+  __syncthreads();
+  // 3) weighted sum of the partial accumulators
   for (int idx = threadIdx.x; idx < G * D; idx += blockDim.x) {
     const int h = idx / D, d = idx % D;
-    float mx = kNegBig;
-    for (int cc = 0; cc < nchunk; ++cc) mx = fmaxf(mx, a.part[((first + cc) * G + h) * (D + 2) + D]);
-    float lsum = 0.0f, asum = 0.0f;
-    for (int cc = 0; cc < nchunk; ++cc) {
-      const float* pp = a.part + ((first + cc) * G + h) * (D + 2);
-      const float f = fast_exp2(pp[D] - mx);
-      lsum += pp[D + 1] * f;
-      asum += pp[d] * f;
+    const float* pp = a.part + (first * G + h) * (D + 2) + d;
+    const int64_t stride = int64_t(G) * (D + 2);
+    float acc0 = 0.0f, acc1 = 0.0f, acc2 = 0.0f, acc3 = 0.0f;
+    int c = 0;
+    for (; c + 4 <= nchunk; c += 4) {
+      acc0 += pp[(c + 0) * stride] * s_w[h][c + 0];
+      acc1 += pp[(c + 1) * stride] * s_w[h][c + 1];
+      acc2 += pp[(c + 2) * stride] * s_w[h][c + 2];
+      acc3 += pp[(c + 3) * stride] * s_w[h][c + 3];
     }
+    for (; c < nchunk; ++c) acc0 += pp[c * stride] * s_w[h][c];
     T* op = static_cast<T*>(a.o) + (int64_t(b) * a.hq + g * G + h) * D + d;
-    *op = static_cast<T>(asum / lsum);
+    *op = static_cast<T>(((acc0 + acc1) + (acc2 + acc3)) * s_inv[h]);
   }
 }
 

@@ -95,7 +95,6 @@ moa_status_t moa_plan(const moa_desc_t* desc, const double* alpha, const double*
   p->desc = d;
   p->group = group;
   p->scale = d.softmax_scale > 0.0f ? d.softmax_scale : static_cast<float>(1.0 / sqrt(double(d.head_dim)));
-  p->decode_chunk = kDecodeChunk;
   const int hkv = d.num_kv_heads;
   p->window.resize(hkv);
   p->capacity.resize(hkv);
@@ -113,6 +112,12 @@ moa_status_t moa_plan(const moa_desc_t* desc, const double* alpha, const double*
     p->capacity[h] = static_cast<int32_t>(w + d.num_sink);
     p->offset[h + 1] = p->offset[h] + p->capacity[h];
   }
+  // Decode split-K chunk: kDecodeChunk slots, doubled until every cache has at
+  // most kMaxMergeChunks chunks.
+  int32_t max_cap = 0;
+  for (int h = 0; h < hkv; ++h) max_cap = std::max(max_cap, p->capacity[h]);
+  p->decode_chunk = kDecodeChunk;
+  while (ceil_div(max_cap, p->decode_chunk) > kMaxMergeChunks) p->decode_chunk *= 2;
   p->kv_order.resize(hkv);
   std::iota(p->kv_order.begin(), p->kv_order.end(), 0);
   std::stable_sort(p->kv_order.begin(), p->kv_order.end(),

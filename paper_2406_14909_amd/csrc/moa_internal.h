@@ -103,6 +103,7 @@ int launch_decode(const DecodeArgs& a, int dtype, int head_dim, int group, void*
 constexpr int kPrefillRows = 128;   // query rows per prefill work-group
 constexpr int kPrefillChunk = 16;   // query tiles per prefill dispatch unit
 constexpr int kNumXcd = 8;          // accelerator dies; work-groups go round-robin over them
-constexpr int kDecodeChunk = 512;   // cache slots per decode work item
+constexpr int kDecodeChunk = 512;   // cache slots per decode work item (minimum)
+constexpr int kMaxMergeChunks = 256;  // split-K chunks per cache the merge kernel stages in LDS
 
 }  // namespace moa

@@ -172,3 +172,11 @@ def test_library_resolves_all_of_its_own_symbols():
                          check=True).stdout
     own = [line for line in out.splitlines() if "moa" in line]
     assert own == [], own
+
+
+def test_decode_geometry_stays_within_merge_limit():
+    # A cache far longer than 256 default chunks still yields a valid workspace size;
+    # the workspace grows with the capacity but not with the number of chunks.
+    long = _plan([float(1 << 27)], [0.0], 1 << 29, 64, hq=8, hkv=1)
+    assert int(long.capacity[0]) == (1 << 27) + 64
+    assert M.moa_decode_workspace_bytes(long, 1) <= 256 * 8 * (128 + 2) * 4

@@ -16,3 +16,20 @@ def test_gpus_above_one_is_refused(monkeypatch, capsys):
     monkeypatch.setattr("sys.argv", ["bench.py", "--gpus", "2"])
     assert bench.main() == 2
     assert "one GPU" in capsys.readouterr().err
+
+
+def test_measured_traffic_needs_matching_sources(tmp_path, monkeypatch):
+    import os
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    src = tmp_path / "paper_2406_14909_amd" / "csrc"
+    src.mkdir(parents=True)
+    (src / "k.hip").write_text("kernel v1")
+    import hashlib
+    h = hashlib.sha256(b"kernel v1").hexdigest()
+    (prof / "t.md").write_text(f"traffic_bytes_per_launch: 1234\nsource_files: k.hip\nsource_sha256: {h}\n")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    assert bench.measured_traffic("t.md") == 1234
+    (src / "k.hip").write_text("kernel v2")
+    assert bench.measured_traffic("t.md") is None
+    assert bench.measured_traffic("missing.md") is None

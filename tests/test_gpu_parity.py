@@ -196,6 +196,7 @@ DECODE_CASES = [
     ("bf16", 2, 4, 2, 64, 0, [1, 3], 10, 5),                   # tiny caches, no sinks
     ("f32", 2, 8, 4, 128, 8, [600, 5, 1, 1200], 1300, 3),      # G = 2 fp32
     ("f32", 1, 4, 4, 64, 2, [1, 2, 3, 4], 1, 6),               # first positions
+    ("bf16", 1, 8, 1, 128, 64, [140000], 140000, 2),          # > 256 default chunks: wider chunks
 ]
 
 
