@@ -154,7 +154,9 @@ moa_status_t moa_prefill(const moa_plan_t* plan, const void* q, const void* k, c
   if (overlaps(o, qbytes, q, qbytes) || overlaps(o, qbytes, k, kbytes) || overlaps(o, qbytes, v, kbytes))
     return fail(MOA_ERR_INVALID_ARG, "moa_prefill: output overlaps an input");
   const int64_t tiles = (n_tokens + kPrefillRows - 1) / kPrefillRows;
-  const int64_t qchunk = std::min<int64_t>(kPrefillChunk, tiles);
+  // A unit spans at least kPrefillUnitBlocks work-groups (query tiles x group),
+  // and at least kPrefillChunk query tiles.
+  const int64_t qchunk = std::min<int64_t>(std::max<int64_t>(kPrefillChunk, kPrefillUnitBlocks / plan->group), tiles);
   const int64_t n_chunks = (tiles + qchunk - 1) / qchunk;
   const int64_t n_units = int64_t(d.num_kv_heads) * batch * n_chunks;
   const int64_t blocks = (n_units + kNumXcd - 1) / kNumXcd * kNumXcd * plan->group * qchunk;

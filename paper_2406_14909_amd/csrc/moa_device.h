@@ -96,6 +96,35 @@ __device__ __forceinline__ void dma16_buf(__amdgpu_buffer_rsrc_t rsrc, uint32_t 
 #endif
 }
 
+// Raw buffer descriptor (4 dwords, wave-uniform) over [base, base + bytes),
+// gfx9-family format; loads at offsets past `bytes` return zeros.
+typedef int32_t i32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ i32x4 make_desc(const void* base, uint32_t bytes) {
+  const uint64_t a = reinterpret_cast<uint64_t>(base);
+  return i32x4{static_cast<int32_t>(a & 0xffffffffu), static_cast<int32_t>((a >> 32) & 0xffffu),
+               static_cast<int32_t>(bytes), 0x00020000};
+}
+
+// Asynchronous 16-byte-per-lane copy from a buffer straight into LDS
+// (buffer_load_dwordx4 ... lds): lane i's bytes land at lds_base + 16 * i.
+// It is issued as an opaque statement, so the compiler neither counts it as an
+// LDS write nor waits for it before unrelated LDS reads; the caller orders it
+// with s_waitcnt vmcnt and a work-group barrier before the data is read.
+__device__ __forceinline__ void dma16_async(i32x4 desc, uint32_t voffset, void* lds_base) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  typedef __attribute__((address_space(3))) char lds_char;
+  const uint32_t lds = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_char*)lds_base));
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(lds), "v"(voffset), "s"(desc)
+               : "memory", "m0");
+#else
+  (void)desc;
+  (void)voffset;
+  (void)lds_base;
+#endif
+}
+
 // DPP lane permutation of a float (no LDS round trip).
 template <int ctrl>
 __device__ __forceinline__ float dpp(float x) {

@@ -101,7 +101,8 @@ int launch_kv_append(const AppendArgs& a, int dtype, int head_dim, void* stream)
 int launch_decode(const DecodeArgs& a, int dtype, int head_dim, int group, void* stream);
 
 constexpr int kPrefillRows = 128;   // query rows per prefill work-group
-constexpr int kPrefillChunk = 16;   // query tiles per prefill dispatch unit
+constexpr int kPrefillChunk = 16;   // minimum query tiles per prefill dispatch unit
+constexpr int kPrefillUnitBlocks = 64;  // minimum work-groups per prefill dispatch unit
 constexpr int kNumXcd = 8;          // accelerator dies; work-groups go round-robin over them
 constexpr int kDecodeChunk = 512;   // cache slots per decode work item (minimum)
 constexpr int kMaxMergeChunks = 256;  // split-K chunks per cache the merge kernel stages in LDS

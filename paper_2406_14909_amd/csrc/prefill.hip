@@ -106,22 +106,21 @@ struct Tiles {
   static constexpr bool kTr = sizeof(T) == 2;        // bf16: V via the transposing read
   static constexpr int RB = D * int(sizeof(T));      // bytes per K/V row
   static constexpr int CPR = RB / 16;                // 16-byte chunks per row
-  static constexpr int TILE_BYTES = BN * RB;         // one V tile (bf16, row-major)
-  // K rows carry one 16-byte padding chunk: stride RBP = RB + 16, so the rows
-  // read together by an MFMA operand load start in different bank groups.
-  static constexpr int RBP = RB + 16;
-  static constexpr int KCH = BN * (CPR + 1);         // 16-byte chunks in a padded K tile
-  static constexpr int K_DMA = (KCH + 63) / 64;      // 1 KB direct-to-LDS loads per K tile
-  static constexpr int K_BYTES = K_DMA * 1024;       // K buffer (slack after the last row)
-  static constexpr int V_DMA_PER_WAVE = TILE_BYTES / 1024 / NW;
+  static constexpr int TILE_BYTES = BN * RB;         // one K (or bf16 V) tile, rows unpadded
+  static constexpr int DMA_PER_WAVE = TILE_BYTES / 1024 / NW;   // 1 KB direct-to-LDS loads
+  // K stages in LDS: bf16 keeps K two tiles ahead (3 buffers, 80 KB per
+  // work-group with V); the fp32 instantiation keeps one tile ahead.
+  static constexpr int KSTAGES = kTr ? 3 : 2;
   static constexpr int EPL = Vec16<T>::N;            // elements per 16-byte chunk
   static constexpr int VT_LD = BN + 4;               // fp32 only: V^T row stride (elements)
   static constexpr int VT_BYTES = D * VT_LD * int(sizeof(T));
   static constexpr int V_BYTES = kTr ? TILE_BYTES : VT_BYTES;
   static constexpr int VREG = kTr ? 1 : BN * CPR / (NW * 64);   // fp32 V chunks staged per thread
-  // V rows (bf16): chunk c of row r sits at chunk position c ^ swz_v(r), which
-  // depends on r mod 8 only; the 4 rows x 4 chunks read by half a wave in one
-  // transposing load then hit 16 different bank groups.
+  // K rows: chunk c of row r sits at chunk position c ^ swz_k(r), so the 16
+  // rows read together by an MFMA operand load hit 16 different bank groups.
+  __device__ __forceinline__ static int swz_k(int r) { return CPR >= 16 ? (r & 15) : ((r >> 1) & 7); }
+  // V rows (bf16): depends on r mod 8 only; the 4 rows x 4 chunks read by half
+  // a wave in one transposing load hit 16 different bank groups.
   __device__ __forceinline__ static int swz_v(int r) { return CPR >= 16 ? 4 * (r & 3) : 4 * ((r >> 1) & 1); }
 };
 
@@ -130,9 +129,9 @@ __global__ void __launch_bounds__(NW * 64, 2) prefill_kernel(PrefillArgs a) {
   using M = Mma<T>;
   using TL = Tiles<T, D>;
   constexpr int KS = D / M::K;            // MFMA steps over the head dimension
-  constexpr int RB = TL::RB, RBP = TL::RBP, CPR = TL::CPR, EPL = TL::EPL;
+  constexpr int RB = TL::RB, CPR = TL::CPR, EPL = TL::EPL, KST = TL::KSTAGES;
 
-  __shared__ __attribute__((aligned(1024))) char sK[2][TL::K_BYTES];
+  __shared__ __attribute__((aligned(1024))) char sK[KST][TL::TILE_BYTES];
   __shared__ __attribute__((aligned(1024))) char sV[2][TL::V_BYTES];
 
   const int lane = threadIdx.x & 63;
@@ -207,63 +206,47 @@ __global__ void __launch_bounds__(NW * 64, 2) prefill_kernel(PrefillArgs a) {
   // carries global chunk p ^ swz_v(r).  Keys past the end re-read the last key
   // (always masked by causality).
   // Per-lane byte offsets of the DMA sources relative to the tile's first key
-  // row (tile independent); rows are kept for the clamped path of a tile that
-  // runs past the last key.
-  constexpr int KI = (TL::K_DMA + NW - 1) / NW;      // K DMA instructions per wave (some idle)
-  uint32_t k_src[KI], v_src[TL::kTr ? TL::V_DMA_PER_WAVE : 1];
-  int k_r[KI], v_r[TL::kTr ? TL::V_DMA_PER_WAVE : 1];
+  // row (tile independent).  DMA instruction I writes tile bytes
+  // [I*1024, I*1024 + 1024): lane L's 16 bytes land at chunk m = I*64 + L, i.e.
+  // row m / CPR, chunk position m % CPR, and carry global chunk
+  // position ^ swz(row).  Wave w issues instructions w*DMA_PER_WAVE + i.
+  constexpr int DPW = TL::DMA_PER_WAVE;
+  uint32_t k_src[DPW], v_src[TL::kTr ? DPW : 1];
+  auto dma_row = [&](int i) { return ((wave * DPW + i) * 64 + lane) / CPR; };
 #pragma unroll
-  for (int i = 0; i < KI; ++i) {
-    const int m = (wave + i * NW) * 64 + lane;
-    const int r = min(m / (CPR + 1), BN - 1);
-    const int c = m % (CPR + 1);
-    k_r[i] = r;
-    k_src[i] = uint32_t(r) * uint32_t(kv_row_bytes) + uint32_t(c < CPR ? c : 0) * 16u;
+  for (int i = 0; i < DPW; ++i) {
+    const int m = (wave * DPW + i) * 64 + lane;
+    const int r = m / CPR, p = m % CPR;
+    k_src[i] = uint32_t(r) * uint32_t(kv_row_bytes) + uint32_t(p ^ TL::swz_k(r)) * 16u;
+    if constexpr (TL::kTr) v_src[i] = uint32_t(r) * uint32_t(kv_row_bytes) + uint32_t(p ^ TL::swz_v(r)) * 16u;
   }
-  if constexpr (TL::kTr) {
+  auto tile_j0 = [&](int it) { return (it < ta ? it : tb + (it - ta)) * BN; };
+  // Tile loads go through a buffer resource that spans exactly the tile's real
+  // key rows (at most BN), so no address outside the inputs is ever touched;
+  // rows past the last key re-read key n-1 (always masked by causality).
+  auto tile_dma = [&](const char* base, const auto& src, int it, char* lds) {
+    const int j0 = tile_j0(it);
+    const int64_t rows = min(int64_t(BN), n - j0);
+    const i32x4 rs = make_desc(base + int64_t(j0) * kv_row_bytes, uint32_t((rows - 1) * kv_row_bytes + RB));
+    if (rows == BN) {
 #pragma unroll
-    for (int i = 0; i < TL::V_DMA_PER_WAVE; ++i) {
-      const int m = (wave * TL::V_DMA_PER_WAVE + i) * 64 + lane;
-      const int r = m / CPR, p = m % CPR;
-      v_r[i] = r;
-      v_src[i] = uint32_t(r) * uint32_t(kv_row_bytes) + uint32_t(p ^ TL::swz_v(r)) * 16u;
+      for (int i = 0; i < DPW; ++i) dma16_async(rs, src[i], lds + (wave * DPW + i) * 1024);
+    } else {
+#pragma unroll
+      for (int i = 0; i < DPW; ++i) {
+        const int r = dma_row(i);
+        const uint32_t off = src[i] - uint32_t(r - min(r, int(rows) - 1)) * uint32_t(kv_row_bytes);
+        dma16_async(rs, off, lds + (wave * DPW + i) * 1024);
+      }
     }
-  }
+  };
+  auto issue_k = [&](int it) { tile_dma(kg, k_src, it, &sK[it % KST][0]); };
   Vec16<T> vreg[TL::VREG];
-  auto issue_tile = [&](int it, int buf) {
-    const int j0 = (it < ta ? it : tb + (it - ta)) * BN;
-    const char* kt = kg + int64_t(j0) * kv_row_bytes;
-    const char* vt = vg + int64_t(j0) * kv_row_bytes;
-    if (int64_t(j0) + BN <= n) {                    // common case: every row is a real key
-#pragma unroll
-      for (int i = 0; i < KI; ++i) {
-        const int inst = wave + i * NW;
-        if (inst < TL::K_DMA) dma16(kt + k_src[i], &sK[buf][inst * 1024]);
-      }
-      if constexpr (TL::kTr) {
-#pragma unroll
-        for (int i = 0; i < TL::V_DMA_PER_WAVE; ++i) {
-          const int inst = wave * TL::V_DMA_PER_WAVE + i;
-          dma16(vt + v_src[i], &sV[buf][inst * 1024]);
-        }
-      }
-    } else {                                         // last tile: rows past the end re-read key n-1
-#pragma unroll
-      for (int i = 0; i < KI; ++i) {
-        const int inst = wave + i * NW;
-        const int64_t extra = (min(int64_t(j0 + k_r[i]), n - 1) - (j0 + k_r[i])) * kv_row_bytes;
-        if (inst < TL::K_DMA) dma16(kt + k_src[i] + extra, &sK[buf][inst * 1024]);
-      }
-      if constexpr (TL::kTr) {
-#pragma unroll
-        for (int i = 0; i < TL::V_DMA_PER_WAVE; ++i) {
-          const int inst = wave * TL::V_DMA_PER_WAVE + i;
-          const int64_t extra = (min(int64_t(j0 + v_r[i]), n - 1) - (j0 + v_r[i])) * kv_row_bytes;
-          dma16(vt + v_src[i] + extra, &sV[buf][inst * 1024]);
-        }
-      }
-    }
-    if constexpr (!TL::kTr) {
+  auto issue_v = [&](int it) {
+    if constexpr (TL::kTr) {
+      tile_dma(vg, v_src, it, &sV[it & 1][0]);
+    } else {
+      const int j0 = tile_j0(it);
 #pragma unroll
       for (int i = 0; i < TL::VREG; ++i) {
         const int idx = threadIdx.x + i * NW * 64;
@@ -288,8 +271,21 @@ __global__ void __launch_bounds__(NW * 64, 2) prefill_kernel(PrefillArgs a) {
   };
 
   // Per-lane byte offsets of the MFMA operand reads (tile independent).
-  // K operand: row lrow (+ 32 * sub), head-dim elements [kk*K + half*K/2, +K/2).
-  const int k_lane = lrow * RBP + half * (M::K / 2) * int(sizeof(T));
+  // K operand: row lrow (+ 32 * sub; the swizzle depends on the row's low bits
+  // only), head-dim elements [kk*K + half*K/2, +K/2).
+  auto k_offset = [&](int kk) {
+    if constexpr (TL::kTr) {
+      return lrow * RB + (((2 * kk + half) ^ TL::swz_k(lrow)) * 16);
+    } else {
+      const int d = 2 * kk + half;
+      return lrow * RB + (((d / 4) ^ TL::swz_k(lrow)) * 16) + (d % 4) * 4;
+    }
+  };
+  int k_off[TL::kTr ? KS : 1];
+  if constexpr (TL::kTr) {
+#pragma unroll
+    for (int kk = 0; kk < KS; ++kk) k_off[kk] = k_offset(kk);
+  }
   // Transposing V read: lane 16G + 4e + a points at row (G/2)*4 + e (+ kb0),
   // bf16 column 32*dt + 16*(G%2) + 4a.
   int v_off[D / 32];
@@ -312,14 +308,35 @@ __global__ void __launch_bounds__(NW * 64, 2) prefill_kernel(PrefillArgs a) {
   float m_run = kNegBig, l_run = 0.0f;
   const int my_row = iw0 + lrow;
 
-  if (ntiles > 0) issue_tile(0, 0);
+  // Pipeline: during tile t, V(t+1) and then K(t+2) stream in; at the top of
+  // tile t only the newest K loads may still be in flight.
+  if (ntiles > 0) {
+    issue_v(0);
+    issue_k(0);
+  }
+  if (ntiles > 1) issue_k(1);
   for (int it = 0; it < ntiles; ++it) {
+    const int j0 = tile_j0(it);
+    if constexpr (KST == 3) {
+      if (it + 1 < ntiles) {
+        // all but the last DPW loads (K(it+1)) have landed: K(it), V(it)
+        __builtin_amdgcn_s_waitcnt(0x0F70 | DPW);
+      } else {
+        __builtin_amdgcn_s_waitcnt(0x0F70);
+      }
+    } else {
+      __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
+    }
+    store_vt(it & 1);
+    __syncthreads();                      // ... for every thread; K(it-1), V(it-1) buffers are free
+    if (it + 1 < ntiles) issue_v(it + 1);
+    if constexpr (KST == 3) {
+      if (it + 2 < ntiles) issue_k(it + 2);
+    } else {
+      if (it + 1 < ntiles) issue_k(it + 1);
+    }
     const int buf = it & 1;
-    const int j0 = (it < ta ? it : tb + (it - ta)) * BN;
-    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0): this thread's loads of tile `it` landed
-    store_vt(buf);
-    __syncthreads();                      // ... for every thread; buffer buf^1 is free again
-    if (it + 1 < ntiles) issue_tile(it + 1, buf ^ 1);
+    const int kbuf = it % KST;
 
     if (!wave_active) continue;
     // Does any (row, key) pair of this wave fall inside the mask?
@@ -332,9 +349,10 @@ __global__ void __launch_bounds__(NW * 64, 2) prefill_kernel(PrefillArgs a) {
     // S^T = K Q^T for two 32-key sub-tiles.
     // Fragments of step kk+1 are read while the MFMAs of step kk run; the two
     // 32-key chains alternate so consecutive MFMAs are independent.
-    const char* kb = &sK[buf][k_lane];
+    const char* kb = &sK[kbuf][0];
     auto kfrag = [&](int kk, int sub) {
-      return *reinterpret_cast<const typename M::frag*>(kb + sub * 32 * RBP + kk * M::K * int(sizeof(T)));
+      const int off = TL::kTr ? k_off[TL::kTr ? kk : 0] : k_offset(kk);
+      return *reinterpret_cast<const typename M::frag*>(kb + sub * 32 * RB + off);
     };
     f32x16 sacc[2] = {f32x16{}, f32x16{}};
     typename M::frag kf[2][2];
