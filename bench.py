@@ -88,6 +88,8 @@ def main() -> int:
     ap.add_argument("--profile-kernel", choices=["decode", "prefill", "append", "copy"], default=None,
                     help="launch only this kernel --reps times on the bench workload (hardware-counter runs)")
     ap.add_argument("--reps", type=int, default=3)
+    ap.add_argument("--peaks", action="store_true",
+                    help="measure practical ceilings: hipBLASLt bf16 GEMM TFLOP/s and streaming-read GB/s")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -97,6 +99,10 @@ def main() -> int:
 
     import numpy as np
     import torch
+
+    if args.peaks:
+        print(json.dumps(measure_peaks()), flush=True)
+        return 0
 
     sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
     import workloads
@@ -243,6 +249,46 @@ def main() -> int:
                                               steps_dec, args.cpu_budget)
     print(json.dumps(result), flush=True)
     return 0
+
+
+def measure_peaks():
+    """Practical ceilings on this GPU, measured with library kernels.
+
+    MFMA: a 16384^3 bf16 GEMM (torch.matmul -> hipBLASLt), best of 5.
+    HBM read: torch.sum over 8 GiB of bf16 (a streaming reduction), best of 5;
+    HBM copy: a 4 GiB device-to-device copy (read + write), best of 5.
+    """
+    import torch
+
+    def best_ms(fn, reps=5):
+        fn()
+        torch.cuda.synchronize()
+        best = float("inf")
+        for _ in range(reps):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            best = min(best, e0.elapsed_time(e1))
+        return best
+
+    n = 16384
+    a = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+    b = torch.randn(n, n, device="cuda", dtype=torch.bfloat16)
+    gemm_ms = best_ms(lambda: torch.matmul(a, b))
+    del a, b
+    big = torch.ones((8 << 30) // 2, device="cuda", dtype=torch.bfloat16)
+    read_ms = best_ms(lambda: big.sum(dtype=torch.float32))
+    del big
+    src = torch.ones((4 << 30) // 2, device="cuda", dtype=torch.bfloat16)
+    dst = torch.empty_like(src)
+    copy_ms = best_ms(lambda: dst.copy_(src))
+    return {
+        "gemm_bf16_16384_tflops": round(2.0 * n ** 3 / (gemm_ms / 1e3) / 1e12, 1),
+        "stream_read_gbs": round((8 << 30) / (read_ms / 1e3) / 1e9, 1),
+        "copy_read_plus_write_gbs": round(2 * (4 << 30) / (copy_ms / 1e3) / 1e9, 1),
+    }
 
 
 def profile_kernel(args, M, plan, q_pre, k_pre, v_pre, o_pre, q_dec, k_dec, v_dec, o_dec, kc, vc, pos,
