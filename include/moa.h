@@ -21,6 +21,9 @@
  *                  of different lengths (paper Appendix "Efficiency
  *                  Experiment Setup": decode over KV caches whose length
  *                  differs across heads).
+ *   moa_kv_append_ragged, moa_decode_ragged
+ *                  the same one-token append and decode with every sequence
+ *                  of the batch at its own position (device position array).
  *
  * Definitions used throughout (s = num_sink, w_g = window of KV head g):
  *   window    w_g = min(max(floor(alpha_g + beta_g * N), 1), N), evaluated
@@ -162,6 +165,28 @@ size_t moa_decode_workspace_bytes(const moa_plan_t* plan, int32_t batch);
 moa_status_t moa_decode(const moa_plan_t* plan, const void* q, const void* k_cache,
                         const void* v_cache, void* o, int32_t batch, int64_t pos,
                         void* workspace, size_t ws_bytes, void* hip_stream);
+
+/* One-token append at per-sequence positions (paper Appendix "Efficiency
+ * Experiment Setup": the newest token replaces the oldest entry beyond the
+ * span; each sequence of a serving batch may be at its own position).
+ * positions: device int32[batch]; sequence b appends the token
+ * k_new/v_new[b] (device [batch, 1, num_kv_heads, head_dim]) at position
+ * positions[b].  A negative position leaves sequence b untouched.  Each
+ * sequence's appends must still be contiguous from 0.  1 <= batch <= 65535. */
+moa_status_t moa_kv_append_ragged(const moa_plan_t* plan, void* k_cache, void* v_cache,
+                                  int32_t* pos_cache, const void* k_new, const void* v_new,
+                                  const int32_t* positions, int32_t batch, void* hip_stream);
+
+/* Decode at per-sequence positions (paper Appendix "Efficiency Experiment
+ * Setup": one query against per-head caches of different lengths).  Same as
+ * moa_decode with sequence b at position positions[b] (device int32[batch]);
+ * must follow moa_kv_append_ragged with the same positions.  A negative
+ * position skips sequence b (its output is not written).  The workspace rules
+ * of moa_decode apply (moa_decode_workspace_bytes covers any positions).
+ * Launches two kernels (the second merges split-K partial results). */
+moa_status_t moa_decode_ragged(const moa_plan_t* plan, const void* q, const void* k_cache,
+                               const void* v_cache, void* o, const int32_t* positions, int32_t batch,
+                               void* workspace, size_t ws_bytes, void* hip_stream);
 
 /* Thread-local message of the calling thread's last non-OK status ("" if none). */
 const char* moa_last_error(void);

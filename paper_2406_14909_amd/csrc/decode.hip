@@ -42,12 +42,13 @@ __global__ void __launch_bounds__(256) decode_kernel(DecodeArgs a) {
 
   const int b = blockIdx.x / a.items_per_seq;
   const int item = blockIdx.x - b * a.items_per_seq;
-  int g = 0;
-  for (int h = 1; h < a.hkv; ++h) g += (item >= a.item_start[h]) ? 1 : 0;
-  const int c = item - a.item_start[g];
-  const int nchunk = a.item_start[g + 1] - a.item_start[g];
+  const ItemGeometry geo = locate_item(a, b, item);
+  if (geo.g < 0) return;                          // past this sequence's items
+  const int g = geo.g;
+  const int c = geo.c;
+  const int nchunk = geo.nchunk;
   const int lo = c * a.chunk;
-  const int hi = min(lo + a.chunk, a.fill[g]);
+  const int hi = min(lo + a.chunk, geo.fill);
 
   const int64_t row0 = int64_t(b) * a.rows_total + a.offset[g];
   const T* kbase = static_cast<const T*>(a.kc) + row0 * D + col * EPL;
@@ -185,9 +186,22 @@ __global__ void __launch_bounds__(256) decode_combine_kernel(DecodeArgs a) {
   __shared__ float s_inv[G];
   const int b = blockIdx.x / a.hkv;
   const int g = blockIdx.x - b * a.hkv;
-  const int nchunk = a.item_start[g + 1] - a.item_start[g];
-  if (nchunk == 1) return;
-  const int64_t first = int64_t(b) * a.items_per_seq + a.item_start[g];
+  int nchunk, first_item;
+  if (a.positions == nullptr) {
+    nchunk = a.item_start[g + 1] - a.item_start[g];
+    first_item = a.item_start[g];
+  } else {
+    const int pos = a.positions[b];
+    first_item = 0;
+    for (int h = 0; h < g; ++h) {
+      const int f = min(pos + 1, a.capacity[h]);
+      first_item += f > 0 ? (f + a.chunk - 1) / a.chunk : 0;
+    }
+    const int f = min(pos + 1, a.capacity[g]);
+    nchunk = f > 0 ? (f + a.chunk - 1) / a.chunk : 0;
+  }
+  if (nchunk <= 1) return;
+  const int64_t first = int64_t(b) * a.items_per_seq + first_item;
   // 1) raw running maxima into LDS
   for (int t = threadIdx.x; t < G * nchunk; t += blockDim.x) {
     const int h = t / nchunk, c = t % nchunk;
@@ -239,7 +253,8 @@ int launch_t(const DecodeArgs& a, void* stream) {
   hipError_t e = hipLaunchKernel(reinterpret_cast<const void*>(&decode_kernel<T, D, G>),
                                  dim3(static_cast<unsigned>(blocks)), dim3(256), args, 0,
                                  static_cast<hipStream_t>(stream));
-  if (e != hipSuccess || blocks == int64_t(a.batch) * a.hkv) return static_cast<int>(e);  // no split
+  if (e != hipSuccess || (a.positions == nullptr && blocks == int64_t(a.batch) * a.hkv))
+    return static_cast<int>(e);  // no cache spans several chunks
   e = hipLaunchKernel(reinterpret_cast<const void*>(&decode_combine_kernel<T, D, G>),
                       dim3(static_cast<unsigned>(a.batch * a.hkv)), dim3(256), args, 0,
                       static_cast<hipStream_t>(stream));

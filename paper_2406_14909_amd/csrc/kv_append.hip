@@ -25,17 +25,23 @@ __global__ void __launch_bounds__(256) kv_append_kernel(AppendArgs a) {
   if (ci >= n_cand) return;
   const int64_t s = a.num_sink;
   const int64_t w = a.window[g];
-  const int64_t n_sink = max(int64_t(0), min(a.end, s) - a.start);
-  int64_t p;
-  if (ci < n_sink) {
-    p = a.start + ci;
+  int64_t p, nrow;
+  if (a.positions != nullptr) {                   // one token per sequence, own position
+    p = a.positions[b];
+    if (p < 0) return;                            // inactive sequence
+    nrow = int64_t(b) * a.hkv + g;
   } else {
-    const int64_t lo = max(max(a.start, s), a.end - w);
-    p = lo + (ci - n_sink);
+    const int64_t n_sink = max(int64_t(0), min(a.end, s) - a.start);
+    if (ci < n_sink) {
+      p = a.start + ci;
+    } else {
+      const int64_t lo = max(max(a.start, s), a.end - w);
+      p = lo + (ci - n_sink);
+    }
+    nrow = (int64_t(b) * (a.end - a.start) + (p - a.start)) * a.hkv + g;
   }
   const int64_t slot = p < s ? p : s + (p - s) % w;
   const int64_t crow = int64_t(b) * a.rows_total + a.offset[g] + slot;
-  const int64_t nrow = (int64_t(b) * (a.end - a.start) + (p - a.start)) * a.hkv + g;
   const u32x4* ksrc = reinterpret_cast<const u32x4*>(static_cast<const char*>(a.kn) + nrow * ROW_BYTES) + col;
   const u32x4* vsrc = reinterpret_cast<const u32x4*>(static_cast<const char*>(a.vn) + nrow * ROW_BYTES) + col;
   u32x4* kdst = reinterpret_cast<u32x4*>(static_cast<char*>(a.kc) + crow * ROW_BYTES) + col;

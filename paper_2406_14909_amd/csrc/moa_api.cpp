@@ -229,6 +229,37 @@ moa_status_t moa_kv_append(const moa_plan_t* plan, void* k_cache, void* v_cache,
   return ok();
 }
 
+moa_status_t moa_kv_append_ragged(const moa_plan_t* plan, void* k_cache, void* v_cache,
+                                  int32_t* pos_cache, const void* k_new, const void* v_new,
+                                  const int32_t* positions, int32_t batch, void* hip_stream) {
+  if (!plan) return fail(MOA_ERR_INVALID_ARG, "moa_kv_append_ragged: null plan");
+  if (!k_cache || !v_cache || !pos_cache || !k_new || !v_new || !positions)
+    return fail(MOA_ERR_INVALID_ARG, "moa_kv_append_ragged: null pointer");
+  if (batch < 1 || batch > 65535)
+    return fail(MOA_ERR_INVALID_ARG, "moa_kv_append_ragged: batch must be in [1, 65535]");
+  if (!aligned16(k_cache) || !aligned16(v_cache) || !aligned16(k_new) || !aligned16(v_new) ||
+      (reinterpret_cast<uintptr_t>(pos_cache) & 3u) || (reinterpret_cast<uintptr_t>(positions) & 3u))
+    return fail(MOA_ERR_INVALID_ARG, "moa_kv_append_ragged: misaligned pointer");
+  const moa_desc_t& d = plan->desc;
+  AppendArgs a;
+  memset(&a, 0, sizeof(a));
+  a.kc = k_cache; a.vc = v_cache; a.pos = pos_cache; a.kn = k_new; a.vn = v_new;
+  a.positions = positions;
+  a.rows_total = plan->offset[d.num_kv_heads];
+  a.batch = batch;
+  a.hkv = d.num_kv_heads;
+  a.num_sink = d.num_sink;
+  for (int h = 0; h <= d.num_kv_heads; ++h) a.cand_start[h] = h;    // one token per head
+  for (int h = 0; h < d.num_kv_heads; ++h) {
+    a.window[h] = plan->window[h];
+    a.offset[h] = plan->offset[h];
+  }
+  a.rows_per_seq = d.num_kv_heads;
+  const int err = launch_kv_append(a, d.dtype, d.head_dim, hip_stream);
+  if (err) return fail(MOA_ERR_HIP, "moa_kv_append_ragged: kernel launch failed (hipError " + std::to_string(err) + ")");
+  return ok();
+}
+
 size_t moa_decode_workspace_bytes(const moa_plan_t* plan, int32_t batch) {
   if (!plan || batch < 1) return 0;
   return decode_workspace_bytes(*plan, batch);
@@ -273,6 +304,48 @@ moa_status_t moa_decode(const moa_plan_t* plan, const void* q, const void* k_cac
   for (int h = 0; h <= d.num_kv_heads; ++h) a.item_start[h] = geo.item_start[h];
   const int err = launch_decode(a, d.dtype, d.head_dim, plan->group, hip_stream);
   if (err) return fail(MOA_ERR_HIP, "moa_decode: kernel launch failed (hipError " + std::to_string(err) + ")");
+  return ok();
+}
+
+moa_status_t moa_decode_ragged(const moa_plan_t* plan, const void* q, const void* k_cache,
+                               const void* v_cache, void* o, const int32_t* positions, int32_t batch,
+                               void* workspace, size_t ws_bytes, void* hip_stream) {
+  if (!plan) return fail(MOA_ERR_INVALID_ARG, "moa_decode_ragged: null plan");
+  if (!q || !k_cache || !v_cache || !o || !positions)
+    return fail(MOA_ERR_INVALID_ARG, "moa_decode_ragged: null pointer");
+  if (batch < 1) return fail(MOA_ERR_INVALID_ARG, "moa_decode_ragged: batch must be >= 1");
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(o) ||
+      (reinterpret_cast<uintptr_t>(positions) & 3u))
+    return fail(MOA_ERR_INVALID_ARG, "moa_decode_ragged: misaligned pointer");
+  const size_t need = decode_workspace_bytes(*plan, batch);
+  if (!workspace || ws_bytes < need)
+    return fail(MOA_ERR_WORKSPACE, "moa_decode_ragged: workspace missing or smaller than moa_decode_workspace_bytes (" +
+                                       std::to_string(need) + " bytes)");
+  if (reinterpret_cast<uintptr_t>(workspace) & 255u)
+    return fail(MOA_ERR_WORKSPACE, "moa_decode_ragged: workspace must be 256-byte aligned");
+  const moa_desc_t& d = plan->desc;
+  DecodeGeometry full;   // geometry of full caches: the grid covers every possible item
+  decode_geometry(*plan, int64_t(1) << 30, &full);
+  if (static_cast<int64_t>(full.items_per_seq) * batch >= (int64_t(1) << 31))
+    return fail(MOA_ERR_UNSUPPORTED, "moa_decode_ragged: too many work items for one launch");
+  DecodeArgs a;
+  memset(&a, 0, sizeof(a));
+  a.q = q; a.kc = k_cache; a.vc = v_cache; a.o = o;
+  a.part = static_cast<float*>(workspace);
+  a.rows_total = plan->offset[d.num_kv_heads];
+  a.batch = batch;
+  a.hq = d.num_q_heads;
+  a.hkv = d.num_kv_heads;
+  a.chunk = plan->decode_chunk;
+  a.items_per_seq = full.items_per_seq;
+  a.scale_log2 = plan->scale * 1.4426950408889634f;
+  a.positions = positions;
+  for (int h = 0; h < d.num_kv_heads; ++h) {
+    a.capacity[h] = plan->capacity[h];
+    a.offset[h] = plan->offset[h];
+  }
+  const int err = launch_decode(a, d.dtype, d.head_dim, plan->group, hip_stream);
+  if (err) return fail(MOA_ERR_HIP, "moa_decode_ragged: kernel launch failed (hipError " + std::to_string(err) + ")");
   return ok();
 }
 

@@ -72,6 +72,7 @@ struct AppendArgs {
   int32_t hkv;
   int32_t num_sink;
   int32_t rows_per_seq;      // slots written per sequence
+  const int32_t* positions;  // per-sequence positions of a one-token append (device), or null
   int32_t cand_start[MOA_MAX_KV_HEADS + 1];
   int32_t window[MOA_MAX_KV_HEADS];
   int64_t offset[MOA_MAX_KV_HEADS];
@@ -88,10 +89,12 @@ struct DecodeArgs {
   int32_t hq;
   int32_t hkv;
   int32_t chunk;             // slots per work item
-  int32_t items_per_seq;
+  int32_t items_per_seq;     // work items per sequence (ragged: at full caches)
   float scale_log2;
+  const int32_t* positions;  // per-sequence positions (device), or null: one position for all
   int32_t fill[MOA_MAX_KV_HEADS];
   int32_t item_start[MOA_MAX_KV_HEADS + 1];
+  int32_t capacity[MOA_MAX_KV_HEADS];
   int64_t offset[MOA_MAX_KV_HEADS];
 };
 

@@ -23,7 +23,8 @@ MOA_MAX_Q_HEADS = 512
 
 EXPORTED = (
     "moa_plan", "moa_plan_tables", "moa_plan_free", "moa_prefill", "moa_kv_append",
-    "moa_decode_workspace_bytes", "moa_decode", "moa_last_error",
+    "moa_decode_workspace_bytes", "moa_decode", "moa_last_error", "moa_kv_append_ragged",
+    "moa_decode_ragged",
 )
 
 
@@ -76,6 +77,10 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.moa_decode_workspace_bytes.restype = ctypes.c_size_t
     lib.moa_decode.argtypes = [vp, vp, vp, vp, vp, i32, i64, vp, ctypes.c_size_t, vp]
     lib.moa_decode.restype = ctypes.c_int
+    lib.moa_kv_append_ragged.argtypes = [vp, vp, vp, vp, vp, vp, vp, i32, vp]
+    lib.moa_kv_append_ragged.restype = ctypes.c_int
+    lib.moa_decode_ragged.argtypes = [vp, vp, vp, vp, vp, vp, i32, vp, ctypes.c_size_t, vp]
+    lib.moa_decode_ragged.restype = ctypes.c_int
     lib.moa_last_error.argtypes = []
     lib.moa_last_error.restype = ctypes.c_char_p
     _lib = lib
@@ -242,4 +247,50 @@ def moa_decode(plan: Plan, q, k_cache, v_cache, pos: int, workspace, o=None, str
     _check(load_library().moa_decode(plan.handle, q.data_ptr(), k_cache.data_ptr(),
                                      v_cache.data_ptr(), o.data_ptr(), bsz, int(pos),
                                      workspace.data_ptr(), nbytes, _stream(q, stream)))
+    return o
+
+
+def _positions(positions, bsz):
+    import torch
+    if positions.dtype != torch.int32 or tuple(positions.shape) != (bsz,) or positions.device.type != "cuda":
+        raise MoaError(MOA_ERR_INVALID_ARG, f"positions: expected a GPU int32 tensor of shape ({bsz},)")
+    if not positions.is_contiguous():
+        raise MoaError(MOA_ERR_INVALID_ARG, "positions: must be contiguous")
+
+
+def moa_kv_append_ragged(plan: Plan, k_cache, v_cache, pos_cache, k_new, v_new, positions,
+                         stream=None) -> None:
+    """One token per sequence at its own position (k_new: [B, 1, H_kv, D]; positions: int32[B])."""
+    import torch
+    bsz = int(k_new.shape[0])
+    dt = plan.torch_dtype
+    _need(k_new, (bsz, 1, plan.num_kv_heads, plan.head_dim), dt, "k_new")
+    _need(v_new, (bsz, 1, plan.num_kv_heads, plan.head_dim), dt, "v_new")
+    _need(k_cache, (bsz, plan.cache_rows, plan.head_dim), dt, "k_cache")
+    _need(v_cache, (bsz, plan.cache_rows, plan.head_dim), dt, "v_cache")
+    _need(pos_cache, (bsz, plan.cache_rows), torch.int32, "pos_cache")
+    _positions(positions, bsz)
+    _check(load_library().moa_kv_append_ragged(plan.handle, k_cache.data_ptr(), v_cache.data_ptr(),
+                                               pos_cache.data_ptr(), k_new.data_ptr(), v_new.data_ptr(),
+                                               positions.data_ptr(), bsz, _stream(k_new, stream)))
+
+
+def moa_decode_ragged(plan: Plan, q, k_cache, v_cache, positions, workspace, o=None, stream=None):
+    """Decode with sequence b at position positions[b] (q, o: [B, H_q, D])."""
+    import torch
+    bsz = int(q.shape[0])
+    dt = plan.torch_dtype
+    _need(q, (bsz, plan.num_q_heads, plan.head_dim), dt, "q")
+    _need(k_cache, (bsz, plan.cache_rows, plan.head_dim), dt, "k_cache")
+    _need(v_cache, (bsz, plan.cache_rows, plan.head_dim), dt, "v_cache")
+    _positions(positions, bsz)
+    if o is None:
+        o = torch.empty_like(q)
+    _need(o, q.shape, dt, "o")
+    if workspace.device.type != "cuda" or not workspace.is_contiguous():
+        raise MoaError(MOA_ERR_WORKSPACE, "workspace must be a contiguous GPU tensor")
+    nbytes = workspace.numel() * workspace.element_size()
+    _check(load_library().moa_decode_ragged(plan.handle, q.data_ptr(), k_cache.data_ptr(),
+                                            v_cache.data_ptr(), o.data_ptr(), positions.data_ptr(), bsz,
+                                            workspace.data_ptr(), nbytes, _stream(q, stream)))
     return o

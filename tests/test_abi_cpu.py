@@ -180,3 +180,16 @@ def test_decode_geometry_stays_within_merge_limit():
     long = _plan([float(1 << 27)], [0.0], 1 << 29, 64, hq=8, hkv=1)
     assert int(long.capacity[0]) == (1 << 27) + 64
     assert M.moa_decode_workspace_bytes(long, 1) <= 256 * 8 * (128 + 2) * 4
+
+
+def test_ragged_entry_points_validate_before_launch():
+    p = _plan([100.0, 200.0], [0.0, 0.0], 1024, 4, hq=4, hkv=2)
+    h = p.handle
+    fake = 1 << 20
+    need = lib.moa_decode_workspace_bytes(h, 2)
+    assert lib.moa_kv_append_ragged(h, fake, fake, fake, fake, fake, None, 2, None) == M.MOA_ERR_INVALID_ARG
+    assert lib.moa_kv_append_ragged(h, fake, fake, fake, fake, fake, fake + 2, 2, None) == M.MOA_ERR_INVALID_ARG
+    assert lib.moa_kv_append_ragged(h, fake, fake, fake, fake, fake, fake, 0, None) == M.MOA_ERR_INVALID_ARG
+    assert lib.moa_decode_ragged(h, fake, fake, fake, fake, None, 2, fake, need, None) == M.MOA_ERR_INVALID_ARG
+    assert lib.moa_decode_ragged(h, fake, fake, fake, fake, fake, 2, fake, need - 1, None) == M.MOA_ERR_WORKSPACE
+    assert lib.moa_decode_ragged(h, fake, fake, fake, fake, fake, 0, fake, need, None) == M.MOA_ERR_INVALID_ARG

@@ -103,7 +103,8 @@ def _elastic(name, hq, hkv, n, mean_frac, prefill_batch, decode_batch, steps, se
 
 
 def workloads() -> List[Workload]:
-    """The five workload shapes (index 0 is the small oracle-checkable case)."""
+    """The workload shapes (index 0 is the small oracle-checkable case; index 5 is
+    the long-context batch-1 decode case)."""
     small = Workload("small-mha4-d64-n512-f32", 4, 4, 64, 4, 512, "f32", 1, 1, 16, 0,
                      (64.0, 128.0, 256.0, 512.0), (0.0, 0.0, 0.0, 0.0))
     return [
@@ -112,6 +113,7 @@ def workloads() -> List[Workload]:
         _elastic("vicuna7b-decode-b32-ctx8192", 32, 32, 8192, 0.5, 32, 32, 256, 2),
         _elastic("llama3-8b-gqa-n16384", 32, 8, 16384, 0.5, 1, 16, 256, 3),
         _elastic("llama3-70b-gqa-n32768", 64, 8, 32768, 0.25, 1, 8, 512, 4),
+        _elastic("vicuna7b-decode-b1-ctx131072", 32, 32, 131072, 0.5, 1, 1, 512, 5),
     ]
 
 
