@@ -24,25 +24,41 @@ moa_status_t ok() { return MOA_OK; }
 
 static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-void decode_geometry(const moa_plan_s& p, int64_t pos, DecodeGeometry* g) {
-  const int hkv = p.desc.num_kv_heads;
-  g->item_start[0] = 0;
-  for (int h = 0; h < hkv; ++h) {
-    const int64_t fill = std::min<int64_t>(pos + 1, p.capacity[h]);
-    g->fill[h] = static_cast<int32_t>(fill);
-    g->item_start[h + 1] = g->item_start[h] + static_cast<int32_t>(ceil_div(fill, p.decode_chunk));
-  }
-  g->items_per_seq = g->item_start[hkv];
+// Workspace: decode partials, fp32 [workers + batch * hkv][group][head_dim + 4]
+// (acc[head_dim], running max m, running sum l, padding), for the largest
+// worker count a launch uses.
+static size_t decode_workspace_bytes(const moa_plan_s& p, int32_t batch) {
+  const size_t rows = static_cast<size_t>(kMaxDecodeWorkers) + static_cast<size_t>(batch) * p.desc.num_kv_heads;
+  return rows * sizeof(float) * static_cast<size_t>(p.group) * (p.desc.head_dim + kDecodePartPad);
 }
 
-// Workspace: split-K partials, fp32 [batch * items][group][head_dim + 2]
-// (acc[head_dim], running max m, running sum l), sized for the largest
-// number of work items (every cache full).
-static size_t decode_workspace_bytes(const moa_plan_s& p, int32_t batch) {
-  int64_t max_items = 0;
-  for (int h = 0; h < p.desc.num_kv_heads; ++h) max_items += ceil_div(p.capacity[h], p.decode_chunk);
-  const size_t per_item = sizeof(float) * static_cast<size_t>(p.group) * (p.desc.head_dim + 2);
-  return per_item * static_cast<size_t>(max_items) * batch;
+// Decode arguments shared by both decode entry points; seg_len[g] is head g's
+// virtual segment per sequence (its fill, or its capacity with per-sequence
+// positions).
+static moa_status_t decode_args(const moa_plan_s& p, const char* who, const void* q, const void* k_cache,
+                                const void* v_cache, void* o, int32_t batch, void* workspace,
+                                const int64_t* seg_len, DecodeArgs* a) {
+  const moa_desc_t& d = p.desc;
+  memset(a, 0, sizeof(*a));
+  a->q = q; a->kc = k_cache; a->vc = v_cache; a->o = o;
+  a->part = static_cast<float*>(workspace);
+  a->rows_total = p.offset[d.num_kv_heads];
+  a->batch = batch;
+  a->hq = d.num_q_heads;
+  a->hkv = d.num_kv_heads;
+  a->scale_log2 = p.scale * 1.4426950408889634f;
+  a->seg_start[0] = 0;
+  for (int h = 0; h < d.num_kv_heads; ++h) {
+    a->seg_start[h + 1] = a->seg_start[h] + seg_len[h];
+    a->capacity[h] = p.capacity[h];
+    a->offset[h] = p.offset[h];
+  }
+  a->seq_keys = a->seg_start[d.num_kv_heads];
+  if (a->seq_keys <= 0 || static_cast<double>(a->seq_keys) * batch >= 9007199254740992.0 ||
+      static_cast<int64_t>(batch) * d.num_kv_heads >= (int64_t(1) << 31))
+    return fail(MOA_ERR_UNSUPPORTED, std::string(who) + ": batch x cache slots too large for one launch");
+  a->total = a->seq_keys * batch;
+  return ok();
 }
 
 static bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; }
@@ -112,12 +128,6 @@ moa_status_t moa_plan(const moa_desc_t* desc, const double* alpha, const double*
     p->capacity[h] = static_cast<int32_t>(w + d.num_sink);
     p->offset[h + 1] = p->offset[h] + p->capacity[h];
   }
-  // Decode split-K chunk: kDecodeChunk slots, doubled until every cache has at
-  // most kMaxMergeChunks chunks.
-  int32_t max_cap = 0;
-  for (int h = 0; h < hkv; ++h) max_cap = std::max(max_cap, p->capacity[h]);
-  p->decode_chunk = kDecodeChunk;
-  while (ceil_div(max_cap, p->decode_chunk) > kMaxMergeChunks) p->decode_chunk *= 2;
   p->kv_order.resize(hkv);
   std::iota(p->kv_order.begin(), p->kv_order.end(), 0);
   std::stable_sort(p->kv_order.begin(), p->kv_order.end(),
@@ -282,26 +292,11 @@ moa_status_t moa_decode(const moa_plan_t* plan, const void* q, const void* k_cac
   if (reinterpret_cast<uintptr_t>(workspace) & 255u)
     return fail(MOA_ERR_WORKSPACE, "moa_decode: workspace must be 256-byte aligned");
   const moa_desc_t& d = plan->desc;
-  DecodeGeometry geo;
-  decode_geometry(*plan, pos, &geo);
-  if (static_cast<int64_t>(geo.items_per_seq) * batch >= (int64_t(1) << 31))
-    return fail(MOA_ERR_UNSUPPORTED, "moa_decode: too many work items for one launch");
+  int64_t seg_len[MOA_MAX_KV_HEADS];
+  for (int h = 0; h < d.num_kv_heads; ++h) seg_len[h] = std::min<int64_t>(pos + 1, plan->capacity[h]);
   DecodeArgs a;
-  memset(&a, 0, sizeof(a));
-  a.q = q; a.kc = k_cache; a.vc = v_cache; a.o = o;
-  a.part = static_cast<float*>(workspace);
-  a.rows_total = plan->offset[d.num_kv_heads];
-  a.batch = batch;
-  a.hq = d.num_q_heads;
-  a.hkv = d.num_kv_heads;
-  a.chunk = plan->decode_chunk;
-  a.items_per_seq = geo.items_per_seq;
-  a.scale_log2 = plan->scale * 1.4426950408889634f;
-  for (int h = 0; h < d.num_kv_heads; ++h) {
-    a.fill[h] = geo.fill[h];
-    a.offset[h] = plan->offset[h];
-  }
-  for (int h = 0; h <= d.num_kv_heads; ++h) a.item_start[h] = geo.item_start[h];
+  const moa_status_t st = decode_args(*plan, "moa_decode", q, k_cache, v_cache, o, batch, workspace, seg_len, &a);
+  if (st != MOA_OK) return st;
   const int err = launch_decode(a, d.dtype, d.head_dim, plan->group, hip_stream);
   if (err) return fail(MOA_ERR_HIP, "moa_decode: kernel launch failed (hipError " + std::to_string(err) + ")");
   return ok();
@@ -324,26 +319,13 @@ moa_status_t moa_decode_ragged(const moa_plan_t* plan, const void* q, const void
   if (reinterpret_cast<uintptr_t>(workspace) & 255u)
     return fail(MOA_ERR_WORKSPACE, "moa_decode_ragged: workspace must be 256-byte aligned");
   const moa_desc_t& d = plan->desc;
-  DecodeGeometry full;   // geometry of full caches: the grid covers every possible item
-  decode_geometry(*plan, int64_t(1) << 30, &full);
-  if (static_cast<int64_t>(full.items_per_seq) * batch >= (int64_t(1) << 31))
-    return fail(MOA_ERR_UNSUPPORTED, "moa_decode_ragged: too many work items for one launch");
+  int64_t seg_len[MOA_MAX_KV_HEADS];
+  for (int h = 0; h < d.num_kv_heads; ++h) seg_len[h] = plan->capacity[h];
   DecodeArgs a;
-  memset(&a, 0, sizeof(a));
-  a.q = q; a.kc = k_cache; a.vc = v_cache; a.o = o;
-  a.part = static_cast<float*>(workspace);
-  a.rows_total = plan->offset[d.num_kv_heads];
-  a.batch = batch;
-  a.hq = d.num_q_heads;
-  a.hkv = d.num_kv_heads;
-  a.chunk = plan->decode_chunk;
-  a.items_per_seq = full.items_per_seq;
-  a.scale_log2 = plan->scale * 1.4426950408889634f;
+  const moa_status_t st =
+      decode_args(*plan, "moa_decode_ragged", q, k_cache, v_cache, o, batch, workspace, seg_len, &a);
+  if (st != MOA_OK) return st;
   a.positions = positions;
-  for (int h = 0; h < d.num_kv_heads; ++h) {
-    a.capacity[h] = plan->capacity[h];
-    a.offset[h] = plan->offset[h];
-  }
   const int err = launch_decode(a, d.dtype, d.head_dim, plan->group, hip_stream);
   if (err) return fail(MOA_ERR_HIP, "moa_decode_ragged: kernel launch failed (hipError " + std::to_string(err) + ")");
   return ok();

@@ -148,40 +148,4 @@ __device__ __forceinline__ float group_sum(float x) {
   return x;
 }
 
-// Split-K geometry of one (sequence, work item): KV head, chunk, chunks of the
-// head and filled slots.  Uniform batches use the host-computed tables; with
-// per-sequence positions it is derived from the sequence's position (a
-// negative position or an item past the sequence's last one gives g = -1).
-struct ItemGeometry {
-  int g, c, nchunk, fill, first_item;
-};
-__device__ __forceinline__ ItemGeometry locate_item(const DecodeArgs& a, int b, int item) {
-  ItemGeometry r{-1, 0, 0, 0, 0};
-  if (a.positions == nullptr) {
-    int g = 0;
-    for (int h = 1; h < a.hkv; ++h) g += (item >= a.item_start[h]) ? 1 : 0;
-    r.g = g;
-    r.first_item = a.item_start[g];
-    r.c = item - r.first_item;
-    r.nchunk = a.item_start[g + 1] - a.item_start[g];
-    r.fill = a.fill[g];
-    return r;
-  }
-  const int pos = a.positions[b];
-  int start = 0;
-  for (int h = 0; h < a.hkv; ++h) {
-    const int f = min(pos + 1, a.capacity[h]);
-    const int nch = f > 0 ? (f + a.chunk - 1) / a.chunk : 0;
-    if (r.g < 0 && item < start + nch) {
-      r.g = h;
-      r.first_item = start;
-      r.c = item - start;
-      r.nchunk = nch;
-      r.fill = f;
-    }
-    start += nch;
-  }
-  return r;
-}
-
 }  // namespace moa

@@ -15,7 +15,6 @@ struct moa_plan_s {
   moa_desc_t desc;
   int32_t group;                   // num_q_heads / num_kv_heads
   float scale;                     // resolved softmax scale
-  int32_t decode_chunk;            // cache slots per decode work item
   std::vector<int32_t> window;     // [H_kv]
   std::vector<int32_t> capacity;   // [H_kv]
   std::vector<int64_t> offset;     // [H_kv + 1]
@@ -27,14 +26,6 @@ namespace moa {
 // Error reporting (thread-local message behind moa_last_error).
 moa_status_t fail(moa_status_t st, const std::string& msg);
 moa_status_t ok();
-
-// Decode split-K geometry for one position (host side).
-struct DecodeGeometry {
-  int32_t fill[MOA_MAX_KV_HEADS];
-  int32_t item_start[MOA_MAX_KV_HEADS + 1];
-  int32_t items_per_seq;
-};
-void decode_geometry(const moa_plan_s& p, int64_t pos, DecodeGeometry* g);
 
 // ---------------------------------------------------------------------------
 // Kernel argument blocks (passed by value; the per-head tables ride along).
@@ -78,22 +69,30 @@ struct AppendArgs {
   int64_t offset[MOA_MAX_KV_HEADS];
 };
 
+// Decode work split: the filled cache slots of every (sequence, KV head) pair,
+// laid end to end in (sequence, head) order, form one virtual key range of
+// `total` keys, cut into `workers` near-equal pieces (one per wave):
+// worker w covers [start(w), start(w + 1)) with
+// start(w) = w * per_worker + (w * rem) / workers.  Head g of a sequence owns
+// virtual keys [seg_start[g], seg_start[g + 1]) of that sequence's range.
 struct DecodeArgs {
   const void* q;
   const void* kc;
   const void* vc;
   void* o;
-  float* part;               // [items][group][D + 2] split-K partials
+  float* part;               // [workers + batch * hkv][group][head_dim + 4] partials
+  const int32_t* positions;  // per-sequence positions (device), or null: one position for all
   int64_t rows_total;        // cache rows per sequence
+  int64_t total;             // virtual keys = batch * seq_keys
+  int64_t seq_keys;          // virtual keys per sequence (= seg_start[hkv])
+  int64_t per_worker;        // total / workers (set by the launcher)
+  int32_t rem;               // total % workers (set by the launcher)
+  int32_t workers;           // set by the launcher
   int32_t batch;
   int32_t hq;
   int32_t hkv;
-  int32_t chunk;             // slots per work item
-  int32_t items_per_seq;     // work items per sequence (ragged: at full caches)
   float scale_log2;
-  const int32_t* positions;  // per-sequence positions (device), or null: one position for all
-  int32_t fill[MOA_MAX_KV_HEADS];
-  int32_t item_start[MOA_MAX_KV_HEADS + 1];
+  int64_t seg_start[MOA_MAX_KV_HEADS + 1];
   int32_t capacity[MOA_MAX_KV_HEADS];
   int64_t offset[MOA_MAX_KV_HEADS];
 };
@@ -101,13 +100,14 @@ struct DecodeArgs {
 // Kernel launchers (return hipError_t as int; 0 = success).
 int launch_prefill(const PrefillArgs& a, int dtype, int head_dim, void* stream);
 int launch_kv_append(const AppendArgs& a, int dtype, int head_dim, void* stream);
-int launch_decode(const DecodeArgs& a, int dtype, int head_dim, int group, void* stream);
+int launch_decode(DecodeArgs a, int dtype, int head_dim, int group, void* stream);
 
 constexpr int kPrefillRows = 128;   // query rows per prefill work-group
 constexpr int kPrefillChunk = 16;   // minimum query tiles per prefill dispatch unit
 constexpr int kPrefillUnitBlocks = 64;  // minimum work-groups per prefill dispatch unit
 constexpr int kNumXcd = 8;          // accelerator dies; work-groups go round-robin over them
-constexpr int kDecodeChunk = 512;   // cache slots per decode work item (minimum)
-constexpr int kMaxMergeChunks = 256;  // split-K chunks per cache the merge kernel stages in LDS
+constexpr int kMaxDecodeWorkers = 8192;  // decode workers (waves) per launch, at most
+constexpr int kDecodeMinKeys = 256;      // virtual keys per decode worker, at least
+constexpr int kDecodePartPad = 4;        // partial row: head_dim sums, m, l, 2 pad floats
 
 }  // namespace moa

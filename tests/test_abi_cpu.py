@@ -147,11 +147,16 @@ def test_gpu_entry_points_validate_before_launch():
     assert lib.moa_decode(h, None, fake, fake, fake, 2, 0, fake, need, None) == M.MOA_ERR_INVALID_ARG
 
 
-def test_decode_workspace_grows_with_batch_and_capacity():
+def test_decode_workspace_size():
+    # Partials for at most 8192 workers plus one per (sequence, KV head), each
+    # group x (head_dim + 4) floats; independent of the cache lengths.
     small = _plan([100.0, 200.0], [0.0, 0.0], 1024, 4, hq=4, hkv=2)
     big = _plan([5000.0, 200.0], [0.0, 0.0], 8192, 4, hq=4, hkv=2)
-    assert M.moa_decode_workspace_bytes(small, 2) < M.moa_decode_workspace_bytes(small, 8)
-    assert M.moa_decode_workspace_bytes(small, 2) < M.moa_decode_workspace_bytes(big, 2)
+    for p in (small, big):
+        for bsz in (1, 2, 8):
+            assert M.moa_decode_workspace_bytes(p, bsz) == (8192 + bsz * 2) * 2 * (128 + 4) * 4
+    gqa = _plan([float(1 << 27)], [0.0], 1 << 29, 64, hq=8, hkv=1, d=64)
+    assert M.moa_decode_workspace_bytes(gqa, 3) == (8192 + 3) * 8 * (64 + 4) * 4
 
 
 def test_binding_fails_loudly_without_library(tmp_path):
@@ -172,14 +177,6 @@ def test_library_resolves_all_of_its_own_symbols():
                          check=True).stdout
     own = [line for line in out.splitlines() if "moa" in line]
     assert own == [], own
-
-
-def test_decode_geometry_stays_within_merge_limit():
-    # A cache far longer than 256 default chunks still yields a valid workspace size;
-    # the workspace grows with the capacity but not with the number of chunks.
-    long = _plan([float(1 << 27)], [0.0], 1 << 29, 64, hq=8, hkv=1)
-    assert int(long.capacity[0]) == (1 << 27) + 64
-    assert M.moa_decode_workspace_bytes(long, 1) <= 256 * 8 * (128 + 2) * 4
 
 
 def test_ragged_entry_points_validate_before_launch():

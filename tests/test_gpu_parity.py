@@ -196,7 +196,12 @@ DECODE_CASES = [
     ("bf16", 2, 4, 2, 64, 0, [1, 3], 10, 5),                   # tiny caches, no sinks
     ("f32", 2, 8, 4, 128, 8, [600, 5, 1, 1200], 1300, 3),      # G = 2 fp32
     ("f32", 1, 4, 4, 64, 2, [1, 2, 3, 4], 1, 6),               # first positions
-    ("bf16", 1, 8, 1, 128, 64, [140000], 140000, 2),          # > 256 default chunks: wider chunks
+    ("bf16", 1, 8, 1, 128, 64, [140000], 140000, 2),          # one cache over ~550 workers
+    ("bf16", 2, 16, 8, 128, 64, [1, 63, 64, 65, 200, 1000, 2500, 40], 2600, 2),  # G = 2 matrix cores
+    ("bf16", 2, 8, 2, 64, 4, [300, 1900], 2000, 3),           # G = 4, head_dim 64
+    ("bf16", 1, 64, 8, 128, 64, [5000, 1, 3000, 64, 700, 4999, 128, 2048], 5100, 2),  # G = 8
+    ("bf16", 4, 16, 2, 64, 3, [1, 2], 5, 4),                  # G = 8, one worker for the batch
+    ("bf16", 8, 8, 8, 128, 64, [3000, 17, 900, 2999, 1, 1500, 333, 2000], 3000, 2),  # many workers
 ]
 
 

@@ -67,9 +67,11 @@ def test_ragged_append_and_decode(dt, hq, hkv, d, s, windows, lengths):
 
 
 def test_ragged_with_equal_positions_matches_uniform_bit_exactly():
+    # With every cache full, both entry points split the same keys the same way.
     _say("ragged == uniform")
-    bsz, hq, hkv, d, s, n0 = 3, 16, 4, 128, 64, 2000
+    bsz, hq, hkv, d, s, n0 = 3, 16, 4, 128, 64, 2100
     plan = M.moa_plan(hq, hkv, d, s, n0, "bf16", [100.0, 700.0, 1500.0, 2000.0], [0.0] * 4)
+    assert n0 >= max(plan.capacity)
     k = workloads.randn((bsz, n0 + 1, hkv, d), 80, torch.bfloat16, "cuda")
     v = workloads.randn((bsz, n0 + 1, hkv, d), 81, torch.bfloat16, "cuda")
     q = workloads.randn((bsz, hq, d), 82, torch.bfloat16, "cuda")
