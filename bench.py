@@ -194,6 +194,13 @@ def main() -> int:
     pre_tflops = prefill_flops / (pre_ms / 1e3) / 1e12
     dec_launch_us = 1e3 * dec_ms / steps_dec
 
+    dname = "bf16" if wl.dtype == "bf16" else "float"
+    dec_kernel = (f"decode_mma_kernel<{D},{group}>" if wl.dtype == "bf16" and group >= 2
+                  else f"decode_valu_kernel<{dname},{D},{group}>")
+    layers = (("vicuna7b", "Vicuna-7B-shaped attention layer"), ("llama3-8b", "Llama-3-8B-shaped attention layer"),
+              ("llama3-70b", "Llama-3-70B-shaped attention layer"))
+    layer = next((text for prefix, text in layers if wl.name.startswith(prefix)), "small attention layer")
+    mean_frac = float(np.mean(windows)) / N
     result = {
         "metric": "decode tokens/s (whole step: plan + prefill + cache fill + decode loop)",
         "value": round(value, 2),
@@ -206,10 +213,10 @@ def main() -> int:
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16" if wl.dtype == "bf16" else "f32",
-        "data": "synthetic: q,k,v ~ N(0,1) seeded; per-KV-head elastic windows (mean N/2)",
+        "data": f"synthetic: q,k,v ~ N(0,1) seeded; per-KV-head elastic windows (mean {mean_frac:.2f} N)",
         "config": {
             "workload": wl.name,
-            "layer": "Vicuna-7B-shaped attention layer",
+            "layer": layer,
             "batch": B, "context": N, "decode_steps": steps_dec,
             "num_q_heads": Hq, "num_kv_heads": Hkv, "head_dim": D, "num_sink": s,
             "mean_window": float(np.mean(windows)),
@@ -222,14 +229,14 @@ def main() -> int:
         "prefill_ms": round(pre_ms, 4),
         "prefill_inband_tflops": round(pre_tflops, 2),
         "roofline": {
-            "kernel": "moa_decode (decode_kernel<bf16,128,1> + decode_combine_kernel), per call",
+            "kernel": f"moa_decode ({dec_kernel} + decode_combine_kernel), per call",
             "bound": "hbm",
             "achieved": round(dec_gbs, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
-            "traffic": measured_traffic("hbm_traffic__decode_kernel__vicuna7b-decode-b32-ctx8192.md"),
-            "traffic_kernel": "decode_kernel<bf16,128,1> (bytes per launch)",
+            "traffic": measured_traffic(f"hbm_traffic__decode_kernel__{wl.name}.md"),
+            "traffic_kernel": f"{dec_kernel} (bytes per launch)",
             "bytes_per_launch": round(dec_bytes_total / steps_dec),
         },
         "roofline_prefill": {
@@ -239,7 +246,7 @@ def main() -> int:
             "peak": BF16_MFMA_PEAK_TFLOPS,
             "unit": "TFLOP/s",
             "frac": round(pre_tflops / BF16_MFMA_PEAK_TFLOPS, 4),
-            "traffic": measured_traffic("hbm_traffic__prefill_kernel__vicuna7b-b32-n8192.md"),
+            "traffic": measured_traffic(f"hbm_traffic__prefill_kernel__{wl.name}.md"),
             "flops_per_launch": prefill_flops,
         },
     }
