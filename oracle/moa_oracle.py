@@ -25,6 +25,18 @@ What it computes, step by step, in the paper's terms:
   Throughput Breakdown"): each KV head keeps at most s + w_g entries; once
   full, the newest token replaces the oldest non-sink entry in place.
 
+Two variants of the paper's own kernel setting (Appendix "Main Setup" and
+"Efficiency Experiment Setup"), selected by arguments:
+
+* span_includes_sinks: the rule gives the whole span S = alpha + beta * N,
+  sinks included (Sec. 3.2: span = sliding window + initially unmasked
+  tokens).  S is floored and clipped to [0, N]; the band is w = S - s, at
+  least 1.
+* block: the band is counted in blocks of `block` tokens (the paper's
+  prefill uses 64-token blocks): query i sees key j iff j <= i and (j < s or
+  i // block - j // block < ceil(w / block)).  Decode keeps the token-exact
+  band, as the paper's cache replaces the oldest token one at a time.
+
 All floating point work is float64 on the exact stored input values.
 
 Parity status: every function here is pinned by the CPU tests (brute force,
@@ -42,9 +54,23 @@ import numpy as np
 # Elastic rule -> per-head window table (Sec. 3.2, Eq. 2; Appendix clipping)
 # ----------------------------------------------------------------------------
 
-def window_ref(alpha: float, beta: float, n: int) -> int:
-    """w = min(max(floor(alpha + beta * N), 1), N), evaluated in IEEE double."""
+def window_ref(alpha: float, beta: float, n: int, num_sink: int = 0,
+               span_includes_sinks: bool = False) -> int:
+    """Band width of one head, from the rule alpha + beta * N in IEEE double.
+
+    Default: w = min(max(floor(alpha + beta * N), 1), N).
+    span_includes_sinks: S = min(max(floor(alpha + beta * N), 0), N) and
+    w = max(S - num_sink, 1).
+    """
     x = float(alpha) + float(beta) * float(n)   # Python floats: no fused multiply-add
+    if span_includes_sinks:
+        if not (x >= 0.0):
+            span = 0
+        elif x >= float(n):
+            span = int(n)
+        else:
+            span = int(math.floor(x))
+        return max(span - int(num_sink), 1)
     if not (x >= 1.0):
         return 1
     if x >= float(n):
@@ -53,9 +79,10 @@ def window_ref(alpha: float, beta: float, n: int) -> int:
 
 
 def plan_ref(alpha: Sequence[float], beta: Sequence[float], n: int,
-             num_sink: int) -> Dict[str, np.ndarray]:
+             num_sink: int, span_includes_sinks: bool = False) -> Dict[str, np.ndarray]:
     """Per-KV-head window, cache capacity (sinks + window) and cache row offset."""
-    window = np.array([window_ref(a, b, n) for a, b in zip(alpha, beta)], dtype=np.int32)
+    window = np.array([window_ref(a, b, n, num_sink, span_includes_sinks) for a, b in zip(alpha, beta)],
+                      dtype=np.int32)
     capacity = (window.astype(np.int64) + int(num_sink)).astype(np.int32)
     offset = np.zeros(len(window) + 1, dtype=np.int64)
     offset[1:] = np.cumsum(capacity.astype(np.int64))
@@ -66,16 +93,28 @@ def plan_ref(alpha: Sequence[float], beta: Sequence[float], n: int,
 # Mask (Sec. 3.2 span definition; Appendix "Attention Mask")
 # ----------------------------------------------------------------------------
 
-def visible(i: int, j: int, w: int, s: int) -> bool:
-    """Key j is visible to query i: causal, and in the sink prefix or the band."""
+def band_blocks(w: int, block: int) -> int:
+    """Band length in blocks: ceil(w / block)."""
+    return -(-int(w) // int(block))
+
+
+def visible(i: int, j: int, w: int, s: int, block: int = 0) -> bool:
+    """Key j is visible to query i: causal, and in the sink prefix or the band
+    (counted in tokens, or in blocks of `block` tokens when block > 0)."""
+    if block:
+        return j <= i and (j < s or i // block - j // block < band_blocks(w, block))
     return j <= i and (j < s or i - j < w)
 
 
-def visible_mask(n_q: int, n_k: int, w: int, s: int, q_start: int = 0) -> np.ndarray:
+def visible_mask(n_q: int, n_k: int, w: int, s: int, q_start: int = 0, block: int = 0) -> np.ndarray:
     """Boolean [n_q, n_k] mask for query positions q_start.. and keys 0..n_k-1."""
     i = np.arange(q_start, q_start + n_q, dtype=np.int64)[:, None]
     j = np.arange(n_k, dtype=np.int64)[None, :]
-    return (j <= i) & ((j < s) | (i - j < w))
+    if block:
+        band = (i // block - j // block) < band_blocks(w, block)
+    else:
+        band = (i - j) < w
+    return (j <= i) & ((j < s) | band)
 
 
 # ----------------------------------------------------------------------------
@@ -104,7 +143,7 @@ def masked_softmax_rows(s_rows: np.ndarray, mask_rows: np.ndarray) -> np.ndarray
 
 
 def attention_ref(q, k, v, window: Sequence[int], num_sink: int,
-                  scale: Optional[float] = None, row_block: int = 1024) -> np.ndarray:
+                  scale: Optional[float] = None, row_block: int = 1024, block: int = 0) -> np.ndarray:
     """Prefill output O [B, n, H_q, D] in float64.
 
     q: [B, n, H_q, D]; k, v: [B, n, H_kv, D]; window: [H_kv] integer windows.
@@ -125,14 +164,14 @@ def attention_ref(q, k, v, window: Sequence[int], num_sink: int,
             for r0 in range(0, n, row_block):
                 r1 = min(n, r0 + row_block)
                 s_rows = (q[b, r0:r1, h, :] @ kg[:r1].T) * sc          # S = Q K^T
-                mask = visible_mask(r1 - r0, r1, int(window[g]), num_sink, r0)
+                mask = visible_mask(r1 - r0, r1, int(window[g]), num_sink, r0, block)
                 a = masked_softmax_rows(s_rows, mask)                  # softmax(S + M)
                 out[b, r0:r1, h, :] = a @ vg[:r1]                      # O = A V
     return out
 
 
 def attention_rows_ref(q, k, v, window: Sequence[int], num_sink: int, b: int, h: int,
-                       rows: Sequence[int], scale: Optional[float] = None) -> np.ndarray:
+                       rows: Sequence[int], scale: Optional[float] = None, block: int = 0) -> np.ndarray:
     """Selected prefill output rows O[b, rows, h, :] in float64 ([len(rows), D]).
 
     Each row i is softmax over its visible set J_i only, so large workloads can
@@ -146,7 +185,7 @@ def attention_rows_ref(q, k, v, window: Sequence[int], num_sink: int, b: int, h:
     out = np.zeros((len(rows), d), dtype=np.float64)
     for r, i in enumerate(rows):
         i = int(i)
-        js = visible_set(i, w, num_sink)
+        js = visible_set(i, w, num_sink, block)
         qi = _as64(q[b, i, h, :])
         kj = _as64(k[b, js, g, :])
         vj = _as64(v[b, js, g, :])
@@ -156,21 +195,28 @@ def attention_rows_ref(q, k, v, window: Sequence[int], num_sink: int, b: int, h:
     return out
 
 
-def visible_set(i: int, w: int, s: int) -> np.ndarray:
-    """J_i = {j <= i : j < s or i - j < w} as sorted int64 indices."""
+def visible_set(i: int, w: int, s: int, block: int = 0) -> np.ndarray:
+    """J_i = {j <= i : j < s or j in the band of i} as sorted int64 indices.
+
+    The band starts at i - w + 1 (tokens) or at the first token of block
+    i // block - ceil(w / block) + 1 (blocks)."""
     sinks = np.arange(0, min(s, i + 1), dtype=np.int64)
-    band = np.arange(max(0, i - w + 1), i + 1, dtype=np.int64)
+    if block:
+        start = (i // block - band_blocks(w, block) + 1) * block
+    else:
+        start = i - w + 1
+    band = np.arange(max(0, start), i + 1, dtype=np.int64)
     return np.union1d(sinks, band)
 
 
 def probabilities_ref(q, k, window: Sequence[int], num_sink: int, b: int, h: int,
-                      scale: Optional[float] = None) -> np.ndarray:
+                      scale: Optional[float] = None, block: int = 0) -> np.ndarray:
     """Full attention-probability matrix A [n, n] of one (batch, query head)."""
     q, k = _as64(q), _as64(k)
     n, d = q.shape[1], q.shape[3]
     g = h // (q.shape[2] // k.shape[2])
     s_all = (q[b, :, h, :] @ k[b, :, g, :].T) * _scale(d, scale)
-    return masked_softmax_rows(s_all, visible_mask(n, n, int(window[g]), num_sink))
+    return masked_softmax_rows(s_all, visible_mask(n, n, int(window[g]), num_sink, 0, block))
 
 
 def decode_ref(q_t, k_hist, v_hist, window: Sequence[int], num_sink: int,

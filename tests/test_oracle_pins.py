@@ -272,3 +272,117 @@ def test_planted_arithmetic_mistakes_are_caught(monkeypatch):
                         lambda s_rows, m: np.exp(np.where(m, s_rows, -np.inf))
                         / np.exp(np.where(m, s_rows, -np.inf)).sum(0, keepdims=True))
     assert caught(om.attention_ref)
+
+
+# ---------------------------------------------------------------------------
+# block-granular band and "span includes sinks" plan mode
+# ---------------------------------------------------------------------------
+
+def _frac(text):
+    num, den = text.split("/")
+    return int(num) / int(den)
+
+
+def test_golden_block_band_uniform_attention():
+    rows = read_golden("block_n16_b4_s2_w6.txt")
+    n, s, w, blk = 16, 2, 6, 4
+    q = np.zeros((1, n, 1, 1))
+    k = _rand((1, n, 1, 1), 30)
+    v = np.arange(n, dtype=np.float64).reshape(1, n, 1, 1)
+    out = om.attention_ref(q, k, v, [w], s, block=blk)
+    mask = om.visible_mask(n, n, w, s, block=blk)
+    for i, (ii, js, mean) in enumerate(rows):
+        assert int(ii) == i
+        expect_set = [int(x) for x in js.split()]
+        assert list(om.visible_set(i, w, s, blk)) == expect_set
+        assert [j for j in range(n) if om.visible(i, j, w, s, blk)] == expect_set
+        assert list(np.nonzero(mask[i])[0]) == expect_set
+        assert out[0, i, 0, 0] == pytest.approx(_frac(mean), abs=1e-14)
+        rows_out = om.attention_rows_ref(q, k, v, [w], s, 0, 0, [i], block=blk)
+        assert rows_out[0, 0] == pytest.approx(_frac(mean), abs=1e-14)
+
+
+def test_golden_span_includes_sinks_rule():
+    for lhs, span, rhs in read_golden("rule_windows_span_sinks.txt"):
+        a, b, n, s = lhs.split()
+        w = om.window_ref(float(a), float(b), int(n), int(s), span_includes_sinks=True)
+        assert w == int(rhs)
+        assert w + int(s) == max(int(span), int(s) + 1)
+    p = om.plan_ref([100.0, 5000.0], [0.0, 0.0], 1000, 64, span_includes_sinks=True)
+    assert list(p["window"]) == [36, 936]
+    assert list(p["capacity"]) == [100, 1000]
+
+
+def test_block_band_against_token_band():
+    # The block band of row i starts at a block boundary: on the last row of a
+    # block it covers the token band (equal to it when w is a multiple of the
+    # block), on the first row it is covered by it, and the counts differ by
+    # less than one block everywhere.
+    n, blk = 300, 64
+    ends, starts = np.arange(blk - 1, n, blk), np.arange(0, n, blk)
+    for w in (1, 5, 63, 64, 65, 128, 200, 256, 299):
+        for s in (0, 3, 64):
+            tok = om.visible_mask(n, n, w, s)
+            blm = om.visible_mask(n, n, w, s, block=blk)
+            assert not np.any(tok[ends] & ~blm[ends])
+            assert not np.any(blm[starts] & ~tok[starts])
+            assert np.abs(blm.sum(axis=1) - tok.sum(axis=1)).max() <= blk - 1
+            if w % blk == 0:
+                assert np.array_equal(tok[ends], blm[ends])
+
+
+def test_block_band_wide_enough_equals_causal_attention():
+    bsz, n, h, d = 1, 70, 2, 8
+    q = _rand((bsz, n, h, d), 31)
+    k = _rand((bsz, n, h, d), 32)
+    v = _rand((bsz, n, h, d), 33)
+    tq, tk, tv = (torch.from_numpy(x).permute(0, 2, 1, 3) for x in (q, k, v))
+    ref = torch.nn.functional.scaled_dot_product_attention(tq, tk, tv, is_causal=True).permute(0, 2, 1, 3).numpy()
+    # 65 tokens round up to 2 blocks of 64: every key of a 70-token prompt is in the band
+    np.testing.assert_allclose(om.attention_ref(q, k, v, [65, 128], 0, block=64), ref, rtol=0, atol=1e-12)
+
+
+def test_block_band_brute_force():
+    # Mask rebuilt from explicit lists of allowed blocks; softmax by Python loops.
+    n, d, blk = 11, 3, 3
+    q = _rand((1, n, 1, d), 34)
+    k = _rand((1, n, 1, d), 35)
+    v = _rand((1, n, 1, d), 36)
+    for w in range(1, n + 2):
+        nb = (w + blk - 1) // blk
+        for s in (0, 1, 3, 5):
+            ref = om.attention_ref(q, k, v, [w], s, block=blk)
+            for i in range(n):
+                blocks = [bb for bb in range(i // blk + 1) if bb > i // blk - nb]
+                keys = sorted({j for bb in blocks for j in range(bb * blk, min(bb * blk + blk, i + 1))}
+                              | set(range(min(s, i + 1))))
+                sc = [sum(q[0, i, 0, x] * k[0, j, 0, x] for x in range(d)) / math.sqrt(d) for j in keys]
+                mx = max(sc)
+                ex = [math.exp(z - mx) for z in sc]
+                for x in range(d):
+                    val = sum(e * v[0, j, 0, x] for e, j in zip(ex, keys)) / sum(ex)
+                    assert abs(val - ref[0, i, 0, x]) < 1e-12
+
+
+def _golden_block_ok(mask_fn):
+    rows = read_golden("block_n16_b4_s2_w6.txt")
+    n, s, w, blk = 16, 2, 6, 4
+    for i, (_, _, mean) in enumerate(rows):
+        keys = [j for j in range(n) if mask_fn(i, j, w, s, blk)]
+        if not keys or abs(sum(keys) / len(keys) - _frac(mean)) > 1e-12:
+            return False
+    return True
+
+
+def test_planted_block_mask_mistakes_are_caught():
+    assert _golden_block_ok(om.visible)
+    mutants = [
+        lambda i, j, w, s, b: j <= i and (j < s or i // b - j // b < w // b),             # floor, not ceil
+        lambda i, j, w, s, b: j <= i and (j < s or i // b - j // b <= -(-w // b)),        # one block too many
+        lambda i, j, w, s, b: j <= i and (j < s or i // b - (j + 1) // b < -(-w // b)),   # key block shifted
+        lambda i, j, w, s, b: j <= i and (j < s or i - j < w),                            # token band
+        lambda i, j, w, s, b: j < s or (j <= i and i // b - j // b < -(-w // b)),         # sinks ignore causality
+        lambda i, j, w, s, b: j // b <= i // b and (j < s or i // b - j // b < -(-w // b)),  # no causality inside the block
+    ]
+    for m in mutants:
+        assert not _golden_block_ok(m)
