@@ -60,8 +60,22 @@ def measured_traffic(profile: str):
     return int(float(fields["traffic_bytes_per_launch"]))
 
 
-def visible_pairs(n: int, w: int, s: int) -> int:
-    """sum_{i<n} |{j <= i : j < s or i - j < w}| (closed form per row)."""
+def visible_pairs(n: int, w: int, s: int, block: int = 0) -> int:
+    """sum_{i<n} |{j <= i : j < s or j in the band of i}| (closed form).
+
+    Token band: i - j < w.  Block band (block > 0): the band of row i starts
+    at bs = max(0, (i // block - ceil(w / block) + 1) * block), so row i sees
+    (i + 1 - bs) band keys plus min(s, bs) sinks before the band; bs is
+    constant over a block of rows."""
+    if block:
+        nb = -(-w // block)
+        total = 0
+        for first in range(0, n, block):
+            last = min(n, first + block)                 # rows [first, last)
+            bs = max(0, (first // block - nb + 1) * block)
+            total += (last * (last + 1) - first * (first + 1)) // 2 - (last - first) * bs
+            total += (last - first) * min(s, bs)
+        return total
     total = 0
     # rows i < w: all i+1 keys visible
     a = min(n, w)
@@ -84,6 +98,10 @@ def main() -> int:
     ap.add_argument("--decode-steps", type=int, default=None)
     ap.add_argument("--workload", default="vicuna7b-decode-b32-ctx8192")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--block-band", action="store_true",
+                    help="prefill band in 64-token blocks (the paper's kernel setting)")
+    ap.add_argument("--span-includes-sinks", action="store_true",
+                    help="the elastic rule gives the whole span, sinks included")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds per oracle leg")
     ap.add_argument("--profile-kernel", choices=["decode", "prefill", "append", "copy"], default=None,
                     help="launch only this kernel --reps times on the bench workload (hardware-counter runs)")
@@ -127,7 +145,9 @@ def main() -> int:
     o_pre = torch.empty_like(q_pre)
     o_dec = torch.empty((B, Hq, D), dtype=dtype, device=dev)
 
-    plan = M.moa_plan(Hq, Hkv, D, s, N, wl.dtype, wl.alpha, wl.beta)
+    flags = (M.MOA_BLOCK_BAND if args.block_band else 0) | (M.MOA_SPAN_INCLUDES_SINKS if args.span_includes_sinks else 0)
+    block = M.MOA_BAND_BLOCK if args.block_band else 0
+    plan = M.moa_plan(Hq, Hkv, D, s, N, wl.dtype, wl.alpha, wl.beta, flags=flags)
     kc, vc, pos = M.new_cache(plan, B)
     ws = M.new_workspace(plan, B)
     windows = [int(x) for x in plan.window]
@@ -137,7 +157,7 @@ def main() -> int:
 
     # ---- algorithmic work -------------------------------------------------
     group = Hq // Hkv
-    prefill_flops = 4.0 * D * B * group * sum(visible_pairs(N, w, s) for w in windows)
+    prefill_flops = 4.0 * D * B * group * sum(visible_pairs(N, w, s, block) for w in windows)
     dec_bytes = []
     for t in range(N, N + steps_dec):
         fills = sum(min(t + 1, c) for c in caps)
@@ -153,7 +173,7 @@ def main() -> int:
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(n_ev)]
 
     def step(record: bool):
-        p = M.moa_plan(Hq, Hkv, D, s, N, wl.dtype, wl.alpha, wl.beta)
+        p = M.moa_plan(Hq, Hkv, D, s, N, wl.dtype, wl.alpha, wl.beta, flags=flags)
         if record:
             ev[0][0].record(stream)
         M.moa_prefill(p, q_pre, k_pre, v_pre, o_pre)
@@ -222,6 +242,8 @@ def main() -> int:
             "mean_window": float(np.mean(windows)),
             "density": float(np.mean(caps)) / N,
             "parallelism": "single GPU",
+            "plan_flags": [name for name, on in (("block_band", args.block_band),
+                                                  ("span_includes_sinks", args.span_includes_sinks)) if on],
         },
         "decode_only_tokens_per_s": round(tokens / (dec_ms / 1e3), 2),
         "decode_kernel_avg_us": round(dec_launch_us, 3),
@@ -252,7 +274,7 @@ def main() -> int:
     }
 
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(wl, plan, q_pre, k_pre, v_pre, q_dec, k_dec, v_dec,
+        result["cpu_baseline"] = cpu_baseline(wl, plan, block, q_pre, k_pre, v_pre, q_dec, k_dec, v_dec,
                                               steps_dec, args.cpu_budget)
     print(json.dumps(result), flush=True)
     return 0
@@ -338,7 +360,7 @@ def profile_kernel(args, M, plan, q_pre, k_pre, v_pre, o_pre, q_dec, k_dec, v_de
     return 0
 
 
-def cpu_baseline(wl, plan, q_pre, k_pre, v_pre, q_dec, k_dec, v_dec, steps_dec, budget):
+def cpu_baseline(wl, plan, block, q_pre, k_pre, v_pre, q_dec, k_dec, v_dec, steps_dec, budget):
     """Times the fp64 oracle on a bounded sample of the same step and scales it.
 
     Sample: prefill rows of sequence 0 (all query heads, rows spread over the
@@ -365,7 +387,7 @@ def cpu_baseline(wl, plan, q_pre, k_pre, v_pre, q_dec, k_dec, v_dec, steps_dec, 
     while time.perf_counter() - t0 < budget:
         rows = np.sort(rng.integers(0, N, 8))
         for h in range(Hq):
-            oracle.attention_rows_ref(qc, kc, vc, plan.window, wl.num_sink, 0, h, rows)
+            oracle.attention_rows_ref(qc, kc, vc, plan.window, wl.num_sink, 0, h, rows, block=block)
         rows_done += len(rows)
     t_row = (time.perf_counter() - t0) / rows_done          # one row, all heads
     # decode tokens of sequence 0 at the first decode position

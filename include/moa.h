@@ -38,6 +38,20 @@
  *   scale     scores are scale * (q . k); scale = 1/sqrt(head_dim) when the
  *             descriptor's softmax_scale is 0.
  *
+ * Plan options (moa_desc_t.flags), the paper's own kernel setting:
+ *   MOA_SPAN_INCLUDES_SINKS  the rule gives the whole span S including the
+ *             sinks (paper Sec. 3.2 and Appendix "Attention Span": span =
+ *             sliding window + initially unmasked tokens):
+ *             S = min(max(floor(alpha_g + beta_g * N), 0), N) and
+ *             w_g = max(S - s, 1).
+ *   MOA_BLOCK_BAND  moa_prefill counts the band in blocks of MOA_BAND_BLOCK
+ *             tokens (paper Appendix "Main Setup": block sliding window of 64
+ *             tokens): i sees j iff j <= i and
+ *             (j < s or i / 64 - j / 64 < ceil(w_g / 64)).  The caches and
+ *             moa_decode keep the token-exact band (the cache replaces the
+ *             oldest token one at a time), so with this option a decode step
+ *             is not the last prefill row.
+ *
  * Layouts (all row-major, contiguous, element type = the plan's dtype):
  *   prefill q, o         [batch, n_tokens, num_q_heads,  head_dim]
  *   prefill k, v, k_new  [batch, n_tokens, num_kv_heads, head_dim]
@@ -104,7 +118,13 @@ typedef struct {
   int64_t n;
   int32_t dtype;             /* moa_dtype_t */
   float softmax_scale;       /* 0 => 1/sqrt(head_dim) */
+  uint32_t flags;            /* MOA_SPAN_INCLUDES_SINKS | MOA_BLOCK_BAND, or 0 */
+  uint32_t reserved;         /* must be 0 */
 } moa_desc_t;
+
+#define MOA_SPAN_INCLUDES_SINKS 1u
+#define MOA_BLOCK_BAND 2u
+#define MOA_BAND_BLOCK 64
 
 typedef struct moa_plan_s moa_plan_t;
 

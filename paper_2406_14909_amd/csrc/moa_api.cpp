@@ -102,6 +102,8 @@ moa_status_t moa_plan(const moa_desc_t* desc, const double* alpha, const double*
     return fail(MOA_ERR_INVALID_ARG, "moa_plan: dtype must be MOA_F32 or MOA_BF16");
   if (!isfinite(d.softmax_scale) || d.softmax_scale < 0.0f)
     return fail(MOA_ERR_INVALID_ARG, "moa_plan: softmax_scale must be finite and >= 0");
+  if ((d.flags & ~(MOA_SPAN_INCLUDES_SINKS | MOA_BLOCK_BAND)) != 0 || d.reserved != 0)
+    return fail(MOA_ERR_INVALID_ARG, "moa_plan: unknown flags or nonzero reserved field");
   for (int h = 0; h < d.num_kv_heads; ++h)
     if (!isfinite(alpha[h]) || !isfinite(beta[h]))
       return fail(MOA_ERR_INVALID_ARG, "moa_plan: alpha and beta must be finite");
@@ -117,13 +119,24 @@ moa_status_t moa_plan(const moa_desc_t* desc, const double* alpha, const double*
   p->offset.assign(hkv + 1, 0);
   const double nd = static_cast<double>(d.n);
   for (int h = 0; h < hkv; ++h) {
-    // Elastic rule alpha + beta * N (paper Sec. 3.2, Eq. 2), floored and clipped to [1, N].
+    // Elastic rule alpha + beta * N (paper Sec. 3.2, Eq. 2), floored.  Default:
+    // the value is the band, clipped to [1, N].  MOA_SPAN_INCLUDES_SINKS: it is
+    // the whole span S (sinks + band, Appendix "Attention Span"), clipped to
+    // [0, N], and the band is S - s, at least 1.
     volatile double prod = beta[h] * nd;   // separate rounding: no fused multiply-add
     const double x = alpha[h] + prod;
     int64_t w;
-    if (!(x >= 1.0)) w = 1;
-    else if (x >= nd) w = d.n;
-    else w = static_cast<int64_t>(floor(x));
+    if (d.flags & MOA_SPAN_INCLUDES_SINKS) {
+      int64_t span;
+      if (!(x >= 0.0)) span = 0;
+      else if (x >= nd) span = d.n;
+      else span = static_cast<int64_t>(floor(x));
+      w = std::max<int64_t>(span - d.num_sink, 1);
+    } else {
+      if (!(x >= 1.0)) w = 1;
+      else if (x >= nd) w = d.n;
+      else w = static_cast<int64_t>(floor(x));
+    }
     p->window[h] = static_cast<int32_t>(w);
     p->capacity[h] = static_cast<int32_t>(w + d.num_sink);
     p->offset[h + 1] = p->offset[h] + p->capacity[h];
@@ -187,8 +200,12 @@ moa_status_t moa_prefill(const moa_plan_t* plan, const void* q, const void* k, c
   a.n_chunks = static_cast<int32_t>(n_chunks);
   a.n_units = static_cast<int32_t>(n_units);
   a.scale_log2 = plan->scale * 1.4426950408889634f;
+  a.band_shift = (d.flags & MOA_BLOCK_BAND) ? 6 : 0;
+  static_assert(MOA_BAND_BLOCK == 64, "band_shift is log2(MOA_BAND_BLOCK)");
   for (int h = 0; h < d.num_kv_heads; ++h) {
-    a.window[h] = plan->window[h];
+    // Band length in tokens, or in blocks of MOA_BAND_BLOCK tokens (rounded up).
+    a.window[h] = (d.flags & MOA_BLOCK_BAND) ? (plan->window[h] + MOA_BAND_BLOCK - 1) / MOA_BAND_BLOCK
+                                             : plan->window[h];
     a.kv_order[h] = plan->kv_order[h];
   }
   const int err = launch_prefill(a, d.dtype, d.head_dim, hip_stream);

@@ -46,7 +46,8 @@ struct PrefillArgs {
   int32_t n_chunks;          // ceil(n_qtiles / qchunk)
   int32_t n_units;           // hkv * batch * n_chunks
   float scale_log2;          // softmax scale * log2(e)
-  int32_t window[MOA_MAX_KV_HEADS];
+  int32_t band_shift;        // the band of row i starts at ((i >> shift) - window + 1) << shift
+  int32_t window[MOA_MAX_KV_HEADS];   // band length in units of 2^band_shift tokens
   int16_t kv_order[MOA_MAX_KV_HEADS];
 };
 

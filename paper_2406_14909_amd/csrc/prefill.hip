@@ -1,6 +1,9 @@
 // Prefill attention with a per-KV-head banded-plus-sink causal mask (paper
 // Sec. 2.1, Eq. 1, with the Sec. 3.2 span: sink prefix + diagonal band of
 // width w_g).  Query i sees key j iff j <= i and (j < s or i - j < w_g).
+// With the block band (paper Appendix "Main Setup": 64-token blocks) the band
+// of row i instead starts at the first token of block i/64 - ceil(w_g/64) + 1;
+// both are "j >= band_start(i)" with band_start(i) = ((i >> sh) - W + 1) << sh.
 //
 // One work-group = 4 waves = 128 query rows of one (sequence, query head);
 // each wave owns 32 rows.  The work-group walks only the 64-key tiles that
@@ -162,7 +165,11 @@ __global__ void __launch_bounds__(NW * 64, 2) prefill_kernel(PrefillArgs a) {
   if (qt >= a.n_qtiles) return;                     // past the last query tile
   const int h = g * a.group + within % a.group;
   const int64_t n = a.n;
-  const int w = a.window[g];
+  // Band of row i: keys from band_start(i) to i; token band (shift 0) or
+  // block band (shift 6: whole 64-token blocks, window counted in blocks).
+  const int wband = a.window[g];
+  const int bsh = a.band_shift;
+  auto band_start = [&](int i) { return ((i >> bsh) - wband + 1) * (1 << bsh); };
   const int s = a.num_sink;
   const float c2 = a.scale_log2;
 
@@ -175,7 +182,7 @@ __global__ void __launch_bounds__(NW * 64, 2) prefill_kernel(PrefillArgs a) {
   // Tiles to visit: sink tiles [0, ta) then band tiles [tb, tl].
   const int ta = (min(s, i1) + BN - 1) / BN;
   const int tl = (i1 - 1) / BN;
-  const int tb = max(ta, max(0, i0 - w + 1) / BN);
+  const int tb = max(ta, max(0, band_start(i0)) / BN);
   const int ntiles = ta + max(0, tl - tb + 1);
 
   const int64_t q_row_stride = int64_t(a.hq) * D;
@@ -341,10 +348,10 @@ __global__ void __launch_bounds__(NW * 64, 2) prefill_kernel(PrefillArgs a) {
     if (!wave_active) continue;
     // Does any (row, key) pair of this wave fall inside the mask?
     const bool any_causal = j0 <= iw1 - 1;
-    const bool any_vis = any_causal && (j0 < s || (iw0 - (j0 + BN - 1)) < w);
+    const bool any_vis = any_causal && (j0 < s || band_start(iw0) <= j0 + BN - 1);
     if (!any_vis) continue;
     const bool all_vis = (j0 + BN - 1 <= iw0) && (iw1 - iw0 == 32) &&
-                         ((j0 + BN <= s) || ((iw1 - 1) - j0 < w));
+                         ((j0 + BN <= s) || band_start(iw1 - 1) <= j0);
 
     // S^T = K Q^T for two 32-key sub-tiles.
     // Fragments of step kk+1 are read while the MFMAs of step kk run; the two
@@ -372,7 +379,7 @@ __global__ void __launch_bounds__(NW * 64, 2) prefill_kernel(PrefillArgs a) {
     if (!all_vis) {
       const int jl = j0 + half * 4;                 // key of register 0 of this lane
       const int hi = my_row < i1 ? my_row - jl : -1;  // causal: key offset <= hi
-      const int band = my_row - w + 1 - jl;           // band: key offset >= band
+      const int band = band_start(my_row) - jl;       // band: key offset >= band
       const int sink = s - jl;                        // sink: key offset < sink
 #pragma unroll
       for (int sub = 0; sub < 2; ++sub) {

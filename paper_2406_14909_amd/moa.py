@@ -37,7 +37,14 @@ class moa_desc_t(ctypes.Structure):
         ("n", ctypes.c_int64),
         ("dtype", ctypes.c_int32),
         ("softmax_scale", ctypes.c_float),
+        ("flags", ctypes.c_uint32),
+        ("reserved", ctypes.c_uint32),
     ]
+
+
+MOA_SPAN_INCLUDES_SINKS = 1
+MOA_BLOCK_BAND = 2
+MOA_BAND_BLOCK = 64
 
 
 class MoaError(RuntimeError):
@@ -144,11 +151,14 @@ class Plan:
 
 def moa_plan(num_q_heads: int, num_kv_heads: int, head_dim: int, num_sink: int, n: int,
              dtype: str, alpha: Sequence[float], beta: Sequence[float],
-             softmax_scale: float = 0.0) -> Plan:
-    """Builds the per-KV-head window / capacity / offset tables (host only)."""
+             softmax_scale: float = 0.0, flags: int = 0) -> Plan:
+    """Builds the per-KV-head window / capacity / offset tables (host only).
+
+    flags: MOA_SPAN_INCLUDES_SINKS and/or MOA_BLOCK_BAND (see include/moa.h)."""
     lib = load_library()
     desc = moa_desc_t(int(num_q_heads), int(num_kv_heads), int(head_dim), int(num_sink), int(n),
-                      MOA_BF16 if dtype in ("bf16", "bfloat16") else MOA_F32, float(softmax_scale))
+                      MOA_BF16 if dtype in ("bf16", "bfloat16") else MOA_F32, float(softmax_scale),
+                      int(flags), 0)
     a = np.ascontiguousarray(alpha, dtype=np.float64)
     b = np.ascontiguousarray(beta, dtype=np.float64)
     if a.shape != (num_kv_heads,) or b.shape != (num_kv_heads,):

@@ -31,8 +31,12 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_desc_struct_layout_matches_header():
-    assert ctypes.sizeof(M.moa_desc_t) == 32
+    assert ctypes.sizeof(M.moa_desc_t) == 40
     assert M.moa_desc_t.n.offset == 16 and M.moa_desc_t.softmax_scale.offset == 28
+    assert M.moa_desc_t.flags.offset == 32 and M.moa_desc_t.reserved.offset == 36
+    text = open(os.path.join(ROOT, "include", "moa.h")).read()
+    for name in ("MOA_SPAN_INCLUDES_SINKS", "MOA_BLOCK_BAND", "MOA_BAND_BLOCK"):
+        assert int(re.search(rf"#define {name} (\d+)", text).group(1)) == getattr(M, name)
 
 
 def _plan(alpha, beta, n, s=64, hq=None, hkv=None, d=128, dtype="bf16"):
@@ -56,6 +60,35 @@ def test_plan_tables_equal_oracle_plan_bit_exact(seed):
     assert np.array_equal(p.capacity, ref["capacity"])
     assert np.array_equal(p.offset, ref["offset"])
     assert p.cache_rows == int(ref["offset"][-1])
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_span_includes_sinks_plan_tables_equal_oracle_bit_exact(seed):
+    rng = np.random.default_rng(100 + seed)
+    hkv = int(rng.integers(1, 65))
+    n = int(rng.integers(1, 1 << 20))
+    s = int(rng.integers(0, 300))
+    alpha = rng.uniform(-2048, 8192, hkv)
+    beta = rng.uniform(0, 1, hkv)
+    alpha[: min(hkv, 4)] = [-2048.0, 0.0, float(s), float(s) + 0.5][: min(hkv, 4)]
+    for flags in (M.MOA_SPAN_INCLUDES_SINKS, M.MOA_SPAN_INCLUDES_SINKS | M.MOA_BLOCK_BAND):
+        p = M.moa_plan(hkv, hkv, 128, s, n, "bf16", alpha, beta, flags=flags)
+        ref = oracle.plan_ref(alpha, beta, n, s, span_includes_sinks=True)
+        assert np.array_equal(p.window, ref["window"])
+        assert np.array_equal(p.capacity, ref["capacity"])
+        assert np.array_equal(p.offset, ref["offset"])
+    # the block band changes only prefill's mask, never the tables
+    q = M.moa_plan(hkv, hkv, 128, s, n, "bf16", alpha, beta, flags=M.MOA_BLOCK_BAND)
+    assert np.array_equal(q.window, oracle.plan_ref(alpha, beta, n, s)["window"])
+
+
+def test_plan_rejects_unknown_flags():
+    for flags, reserved in ((4, 0), (1 << 31, 0), (0, 1)):
+        desc = M.moa_desc_t(4, 4, 128, 4, 512, M.MOA_BF16, 0.0, flags, reserved)
+        a = (ctypes.c_double * 4)(*([16.0] * 4))
+        out = ctypes.c_void_p(1)
+        assert lib.moa_plan(ctypes.byref(desc), a, a, ctypes.byref(out)) == M.MOA_ERR_INVALID_ARG
+        assert out.value is None
 
 
 def test_plan_rounding_edges():

@@ -12,6 +12,13 @@ def test_visible_pairs_matches_mask_count(n, w, s):
     assert bench.visible_pairs(n, w, s) == int(oracle.visible_mask(n, n, w, s).sum())
 
 
+@pytest.mark.parametrize("n,w,s", [(1, 1, 0), (7, 3, 2), (200, 1, 0), (200, 64, 64), (200, 65, 3),
+                                   (300, 130, 70), (129, 1000, 0), (64, 63, 5)])
+def test_block_visible_pairs_matches_mask_count(n, w, s):
+    assert bench.visible_pairs(n, w, s, 64) == int(oracle.visible_mask(n, n, w, s, block=64).sum())
+    assert bench.visible_pairs(n, w, s, 4) == int(oracle.visible_mask(n, n, w, s, block=4).sum())
+
+
 def test_gpus_above_one_is_refused(monkeypatch, capsys):
     monkeypatch.setattr("sys.argv", ["bench.py", "--gpus", "2"])
     assert bench.main() == 2

@@ -99,6 +99,68 @@ def test_prefill_is_deterministic():
     assert torch.equal(bits(o1), bits(o2))
 
 
+BLOCK_CASES = [
+    # dtype, B, n, Hq, Hkv, D, sinks, windows (band counted in 64-token blocks)
+    ("bf16", 1, 700, 8, 2, 128, 64, [1, 200]),
+    ("bf16", 2, 333, 4, 4, 64, 64, [63, 64, 65, 128]),
+    ("f32", 1, 300, 4, 2, 128, 3, [5, 130]),
+    ("bf16", 1, 1100, 16, 2, 128, 64, [96, 640]),
+    ("bf16", 1, 129, 2, 2, 128, 0, [64, 1000]),
+    ("bf16", 3, 520, 8, 8, 128, 10, [1, 64, 127, 128, 129, 256, 300, 520]),
+]
+
+
+@pytest.mark.parametrize("case", BLOCK_CASES, ids=lambda c: f"{c[0]}-B{c[1]}-n{c[2]}-hq{c[3]}-hkv{c[4]}-d{c[5]}-s{c[6]}")
+def test_prefill_block_band_matches_oracle(case):
+    dt, bsz, n, hq, hkv, d, s, windows = case
+    _say("prefill block band", case)
+    dtype = DT[dt]
+    plan = M.moa_plan(hq, hkv, d, s, n, dt, [float(w) for w in windows], [0.0] * hkv, flags=M.MOA_BLOCK_BAND)
+    assert list(plan.window) == [min(w, n) for w in windows]
+    q, k, v = _inputs(bsz, n, hq, hkv, d, dtype, 200 + n)
+    o, buf = guarded_empty(q.shape, dtype)
+    M.moa_prefill(plan, q, k, v, o)
+    torch.cuda.synchronize()
+    assert guard_intact(buf, q.shape), "write past the output"
+    ref = oracle.attention_ref(q, k, v, plan.window, s, block=64)
+    assert_close(o, ref, dtype, with_rounding=True, what=f"block prefill {case}")
+
+
+def test_span_includes_sinks_prefill_and_decode():
+    _say("span includes sinks")
+    alpha, beta, n, s = [100.0, 10.0, 5000.0, 300.5], [0.0, 0.0, 0.0, 0.1], 900, 64
+    plan = M.moa_plan(8, 4, 128, s, n, "bf16", alpha, beta, flags=M.MOA_SPAN_INCLUDES_SINKS)
+    windows = oracle.plan_ref(alpha, beta, n, s, span_includes_sinks=True)["window"]
+    assert list(plan.window) == [36, 1, 836, 326]
+    assert np.array_equal(plan.window, windows)
+    q, k, v = _inputs(2, n + 1, 8, 4, 128, torch.bfloat16, 77)
+    o = M.moa_prefill(plan, q[:, :n].contiguous(), k[:, :n].contiguous(), v[:, :n].contiguous())
+    kc, vc, pos = M.new_cache(plan, 2)
+    ws = M.new_workspace(plan, 2)
+    M.moa_kv_append(plan, kc, vc, pos, k[:, :n].contiguous(), v[:, :n].contiguous(), 0)
+    M.moa_kv_append(plan, kc, vc, pos, k[:, n:].contiguous(), v[:, n:].contiguous(), n)
+    od = M.moa_decode(plan, q[:, n].contiguous(), kc, vc, n, ws)
+    torch.cuda.synchronize()
+    assert_close(o, oracle.attention_ref(q[:, :n], k[:, :n], v[:, :n], windows, s), torch.bfloat16,
+                 with_rounding=True, what="span prefill")
+    assert_close(od, oracle.decode_ref(q[:, n], k, v, windows, s), torch.bfloat16, with_rounding=True,
+                 what="span decode")
+
+
+def test_block_band_leaves_decode_token_exact():
+    _say("block band decode")
+    n, s, windows = 300, 4, [70, 129]
+    plan = M.moa_plan(4, 2, 128, s, n, "bf16", [float(w) for w in windows], [0.0, 0.0], flags=M.MOA_BLOCK_BAND)
+    q, k, v = _inputs(1, n, 4, 2, 128, torch.bfloat16, 78)
+    kc, vc, pos = M.new_cache(plan, 1)
+    ws = M.new_workspace(plan, 1)
+    M.moa_kv_append(plan, kc, vc, pos, k.contiguous(), v.contiguous(), 0)
+    od = M.moa_decode(plan, q[:, n - 1].contiguous(), kc, vc, n - 1, ws)
+    torch.cuda.synchronize()
+    assert_close(od, oracle.decode_ref(q[:, n - 1], k, v, windows, s), torch.bfloat16, with_rounding=True,
+                 what="block-band plan decode")
+
+
 # ---------------------------------------------------------------------------
 # KV append / evict (bit-exact)
 # ---------------------------------------------------------------------------

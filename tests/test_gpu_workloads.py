@@ -28,17 +28,22 @@ def _sample_rows(n, w, s, rng, extra=6):
     return sorted(x for x in cand if 0 <= x < n)
 
 
-def _check_prefill_rows(wl, q, k, v, o, plan, b_list, heads, rng):
+def _check_prefill_rows(wl, q, k, v, o, plan, b_list, heads, rng, block=0):
     group = wl.num_q_heads // wl.num_kv_heads
     worst = 0.0
     for b in b_list:
         for h in heads:
             g = h // group
             rows = _sample_rows(int(q.shape[1]), int(plan.window[g]), wl.num_sink, rng)
+            if block:   # first and last rows of the blocks around the band edge
+                w = int(plan.window[g])
+                rows = sorted(set(rows) | {x for e in (w, w + 64, q.shape[1] // 2)
+                                           for x in (e - e % 64, e - e % 64 + 63) if 0 <= x < q.shape[1]})
             qc = q[b:b + 1, :, h:h + 1].cpu()
             kc = k[b:b + 1, :, g:g + 1].cpu()
             vc = v[b:b + 1, :, g:g + 1].cpu()
-            ref = oracle.attention_rows_ref(qc, kc, vc, [int(plan.window[g])], wl.num_sink, 0, 0, rows)
+            ref = oracle.attention_rows_ref(qc, kc, vc, [int(plan.window[g])], wl.num_sink, 0, 0, rows,
+                                            block=block)
             got = o[b, rows, h].cpu()
             worst = max(worst, assert_close(got, ref, torch.bfloat16, what=f"{wl.name} b={b} h={h}"))
     return worst
@@ -59,6 +64,28 @@ def test_prefill_workload_sampled(idx):
     rng = np.random.default_rng(idx)
     heads = list(range(wl.num_q_heads)) if wl.num_q_heads <= 32 else list(range(0, wl.num_q_heads, 3))
     worst = _check_prefill_rows(wl, q, k, v, o, plan, [0], heads, rng)
+    _say("max err", worst)
+
+
+@pytest.mark.parametrize("idx", [1, 4])
+def test_prefill_workload_block_band_sampled(idx):
+    """The paper's kernel setting: rule = whole span (sinks included), band in
+    64-token blocks, at the full workload size."""
+    wl = workloads.workload(idx)
+    bsz, n = wl.prefill_batch, wl.n
+    _say("prefill block band", wl.name, f"B={bsz} n={n}")
+    plan = M.moa_plan(wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.num_sink, n, wl.dtype,
+                      wl.alpha, wl.beta, flags=M.MOA_BLOCK_BAND | M.MOA_SPAN_INCLUDES_SINKS)
+    ref_plan = oracle.plan_ref(wl.alpha, wl.beta, n, wl.num_sink, span_includes_sinks=True)
+    assert np.array_equal(plan.window, ref_plan["window"])
+    q = workloads.randn((bsz, n, wl.num_q_heads, wl.head_dim), 1100 + idx, torch.bfloat16, "cuda")
+    k = workloads.randn((bsz, n, wl.num_kv_heads, wl.head_dim), 2100 + idx, torch.bfloat16, "cuda")
+    v = workloads.randn((bsz, n, wl.num_kv_heads, wl.head_dim), 3100 + idx, torch.bfloat16, "cuda")
+    o = M.moa_prefill(plan, q, k, v)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng(50 + idx)
+    heads = list(range(0, wl.num_q_heads, 2))
+    worst = _check_prefill_rows(wl, q, k, v, o, plan, [0], heads, rng, block=64)
     _say("max err", worst)
 
 
