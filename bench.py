@@ -106,6 +106,10 @@ def main() -> int:
     ap.add_argument("--profile-kernel", choices=["decode", "prefill", "append", "copy"], default=None,
                     help="launch only this kernel --reps times on the bench workload (hardware-counter runs)")
     ap.add_argument("--reps", type=int, default=3)
+    ap.add_argument("--influence", action="store_true",
+                    help="time the attention-influence profile (moa_influence) on the workload's layer shape")
+    ap.add_argument("--influence-n", type=int, default=8192, help="profiled length for --influence")
+    ap.add_argument("--influence-items", type=int, default=4, help="calibration items for --influence")
     ap.add_argument("--peaks", action="store_true",
                     help="measure practical ceilings: hipBLASLt bf16 GEMM TFLOP/s and streaming-read GB/s")
     args = ap.parse_args()
@@ -120,6 +124,9 @@ def main() -> int:
 
     if args.peaks:
         print(json.dumps(measure_peaks()), flush=True)
+        return 0
+    if args.influence:
+        print(json.dumps(measure_influence(args)), flush=True)
         return 0
 
     sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
@@ -278,6 +285,48 @@ def main() -> int:
                                               steps_dec, args.cpu_budget)
     print(json.dumps(result), flush=True)
     return 0
+
+
+def measure_influence(args):
+    """Times moa_influence (dense causal attention of the workload's layer shape,
+    bf16) over a batch of calibration items.  Algorithmic work: two passes of
+    two products (Q K^T and dO V^T), 8 * head_dim flops per causal (query,
+    key) pair per item and query head."""
+    import torch
+
+    sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+    import workloads
+    from paper_2406_14909_amd import moa as M
+
+    wl = workloads.workload(args.workload)
+    n, items, hq, hkv, d = args.influence_n, args.influence_items, wl.num_q_heads, wl.num_kv_heads, wl.head_dim
+    q = workloads.randn((items, n, hq, d), 11, torch.bfloat16, "cuda")
+    k = workloads.randn((items, n, hkv, d), 12, torch.bfloat16, "cuda")
+    v = workloads.randn((items, n, hkv, d), 13, torch.bfloat16, "cuda")
+    do = workloads.randn((items, n, hq, d), 14, torch.bfloat16, "cuda")
+    ebar = M.moa_influence(q, k, v, do)
+    for _ in range(max(1, args.warmup)):
+        M.moa_influence(q, k, v, do, ebar)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        M.moa_influence(q, k, v, do, ebar)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    flops = 8.0 * d * (n * (n + 1) // 2) * hq * items
+    return {
+        "metric": "attention-influence profile throughput", "unit": "TFLOP/s",
+        "value": round(flops / (ms / 1e3) / 1e12, 2), "ms_per_call": round(ms, 3),
+        "config": {"workload": wl.name, "n": n, "items": items, "num_q_heads": hq, "num_kv_heads": hkv,
+                   "head_dim": d},
+        "roofline": {"kernel": f"influence_kernel<{d}>", "bound": "mfma",
+                     "achieved": round(flops / (ms / 1e3) / 1e12, 2), "peak": BF16_MFMA_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(flops / (ms / 1e3) / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4),
+                     "flops_per_launch": flops},
+    }
 
 
 def measure_peaks():

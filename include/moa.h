@@ -24,6 +24,9 @@
  *   moa_kv_append_ragged, moa_decode_ragged
  *                  the same one-token append and decode with every sequence
  *                  of the batch at its own position (device position array).
+ *   moa_influence  the profiling step that precedes the rule search: the
+ *                  block-averaged attention influence of dense attention
+ *                  (paper Sec. 3.3, Eq. 3).
  *
  * Definitions used throughout (s = num_sink, w_g = window of KV head g):
  *   window    w_g = min(max(floor(alpha_g + beta_g * N), 1), N), evaluated
@@ -207,6 +210,26 @@ moa_status_t moa_kv_append_ragged(const moa_plan_t* plan, void* k_cache, void* v
 moa_status_t moa_decode_ragged(const moa_plan_t* plan, const void* q, const void* k_cache,
                                const void* v_cache, void* o, const int32_t* positions, int32_t batch,
                                void* workspace, size_t ws_bytes, void* hip_stream);
+
+/* Attention-influence profile of dense causal attention (paper Sec. 3.3
+ * "Attention Influence Profiling", Eq. 3; Appendix "Derivation of Attention
+ * Influence"; 64-token block granularity per Appendix "Main Setup").
+ * For each calibration item b and query head h, with A = softmax(scale *
+ * Q K^T) under the causal mask, O = A V and the gradient dout = dL/dO of some
+ * loss L, dL/dA = dout V^T and the influence of masking A_ij is
+ *   E_ij = -A_ij / (1 - A_ij) * (G_ij - sum_n G_in A_in),   G = dL/dA
+ * (0 where A_ij is 0 or rounds to 1 in fp32).  Writes the mean of E over the
+ * batch and over each 64 x 64 block (edge blocks: over the entries that
+ * exist; blocks above the diagonal are 0):
+ *   ebar  fp32 [num_q_heads, nb, nb], nb = ceil(n / 64), caller-owned device.
+ * q, dout  [batch, n, num_q_heads,  head_dim]  (bf16, 16-byte aligned)
+ * k, v     [batch, n, num_kv_heads, head_dim]  (bf16, 16-byte aligned)
+ * desc: the layer (num_q_heads, num_kv_heads, head_dim, softmax_scale; dtype
+ * must be MOA_BF16; num_sink, n and flags are ignored: the profiled
+ * attention is dense).  1 <= n <= 65536, batch >= 1.  Allocates nothing;
+ * one kernel launch; the result does not depend on the launch order. */
+moa_status_t moa_influence(const moa_desc_t* desc, const void* q, const void* k, const void* v,
+                           const void* dout, float* ebar, int32_t batch, int64_t n, void* hip_stream);
 
 /* Thread-local message of the calling thread's last non-OK status ("" if none). */
 const char* moa_last_error(void);

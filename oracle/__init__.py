@@ -1,6 +1,6 @@
 """fp64 CPU oracle for MoA attention (test infrastructure only; never on the product path)."""
 from .influence_oracle import (block_average_ref, causal_probabilities, grad_wrt_probabilities,
-                               influence_profile_ref, influence_ref)
+                               influence_profile_ref, influence_ref, influence_rows_ref)
 from .moa_oracle import (CacheModel, attention_ref, attention_rows_ref, cache_contents_ref,
                          cache_ref, decode_ref, masked_softmax_rows, plan_ref,
                          probabilities_ref, visible, visible_mask, visible_set, window_ref)
@@ -8,6 +8,6 @@ from .moa_oracle import (CacheModel, attention_ref, attention_rows_ref, cache_co
 __all__ = [
     "CacheModel", "attention_ref", "attention_rows_ref", "block_average_ref", "cache_contents_ref",
     "cache_ref", "causal_probabilities", "decode_ref", "grad_wrt_probabilities",
-    "influence_profile_ref", "influence_ref", "masked_softmax_rows", "plan_ref",
+    "influence_profile_ref", "influence_ref", "influence_rows_ref", "masked_softmax_rows", "plan_ref",
     "probabilities_ref", "visible", "visible_mask", "visible_set", "window_ref",
 ]

@@ -99,3 +99,26 @@ def influence_profile_ref(q, k, v, dout, scale: Optional[float] = None, block: i
     a = causal_probabilities(q, k, scale)
     g = grad_wrt_probabilities(v, dout, a.shape[1])
     return block_average_ref(influence_ref(a, g), block)
+
+
+def influence_rows_ref(q, k, v, dout, b: int, h: int, rows, scale: Optional[float] = None) -> np.ndarray:
+    """E[b, h, rows, :] ([len(rows), n]) of dense causal attention, each row from
+    its own softmax and its own dL/dA row, so long inputs can be checked on
+    sampled row blocks."""
+    d = q.shape[-1]
+    n = q.shape[1]
+    group = q.shape[2] // k.shape[2]
+    g = h // group
+    sc = 1.0 / math.sqrt(d) if not scale else float(scale)
+    kg, vg = _as64(k[b, :, g, :]), _as64(v[b, :, g, :])
+    out = np.zeros((len(rows), n), dtype=np.float64)
+    for r, i in enumerate(rows):
+        i = int(i)
+        s = (kg[: i + 1] @ _as64(q[b, i, h, :])) * sc
+        e = np.exp(s - s.max())
+        a_row = np.zeros(n)
+        a_row[: i + 1] = e / e.sum()
+        g_row = vg @ _as64(dout[b, i, h, :])
+        out[r] = influence_ref(a_row[None, :], g_row[None, :])[0]
+    return out
+

@@ -1,0 +1,247 @@
+// Attention-influence profiling (paper Sec. 3.3 "Attention Influence
+// Profiling", Eq. 3; Appendix "Derivation of Attention Influence"), fused.
+//
+// For dense causal attention A = softmax(scale * Q K^T) of every query head
+// and a loss that reaches A through O = A V, dL/dA = dO V^T.  The influence
+// of masking A_ij (first-order change of the loss, row renormalised) is
+//     E_ij = -A_ij / (1 - A_ij) * (G_ij - D_i),   G = dO V^T,
+//     D_i  = sum_n G_in A_in,
+// and the profile keeps only its mean over 64 x 64 blocks and over the batch
+// of calibration items.  Neither A nor G is ever stored: per 128-row tile of
+// one query head the work-group makes two passes over the causal key tiles,
+//   pass 1: S = Q K^T, dP = dO V^T; online row max m, row sum l of
+//           e = exp(S - m) and u = sum e * dP, so D_i = u / l and
+//           log-sum-exp = m + log l;
+//   pass 2: S and dP again, P = exp(S - lse), E as above, summed per
+//           (64-row block, 64-key block) into LDS,
+// for every calibration item in turn, then writes the block means.
+//
+// Matrix-core formulation (CDNA4 32x32x16 bf16 MFMA): S^T = K Q^T and
+// dP^T = V dO^T with the K / V tile rows as the A operand (from LDS, rows
+// padded to 272 bytes) and Q^T / dO^T kept in registers, so lane l holds
+// query row l % 32 for 16 keys and row reductions need one cross-lane step.
+// Where fp32 rounds A_ij to 1 (the row's other weights are below 2^-24 of
+// it, e.g. row 0) the influence is reported as 0.
+#include "moa_device.h"
+
+namespace moa {
+
+namespace {
+
+constexpr int IBM = 128;   // query rows per work-group
+constexpr int IBN = 64;    // keys per tile (= profiling block)
+constexpr int INW = 4;     // waves per work-group
+constexpr int kMaxBlocks = kMaxInfluenceN / kInfluenceBlock;
+static_assert(IBN == kInfluenceBlock, "one key tile per profiling block");
+
+__device__ __forceinline__ f32x16 mma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+#else
+  (void)a;
+  (void)b;
+  return c;
+#endif
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+  x = group_sum<16>(x);
+  x += __shfl_xor(x, 16, 64);
+  x += __shfl_xor(x, 32, 64);
+  return x;
+}
+
+template <int D>
+__global__ void __launch_bounds__(INW * 64, 2) influence_kernel(InfluenceArgs a) {
+  constexpr int KS = D / 16;              // MFMA steps over the head dimension
+  constexpr int RB = D * 2;               // bytes per K / V row
+  constexpr int RS = RB + 16;             // padded LDS row stride
+  constexpr int CPR = RB / 16;            // 16-byte chunks per row
+  constexpr int LPT = IBN * CPR / (INW * 64);   // chunks per thread per tile
+
+  __shared__ __attribute__((aligned(16))) char sK[IBN * RS];
+  __shared__ __attribute__((aligned(16))) char sV[IBN * RS];
+  __shared__ float s_part[INW][kMaxBlocks];     // per-wave block sums
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int lrow = lane & 31;
+  const int half = lane >> 5;
+
+  // Heaviest row tiles (most key tiles) first.
+  const int h = static_cast<int>(blockIdx.x) % a.hq;
+  const int t = a.n_tiles - 1 - static_cast<int>(blockIdx.x) / a.hq;
+  const int g = h / a.group;
+  const int n = a.n;
+  const int i0 = t * IBM;
+  const int i1 = min(n, i0 + IBM);
+  const int iw0 = i0 + wave * 32;
+  const bool wave_active = iw0 < i1;
+  const int iw_last = min(i1, iw0 + 32) - 1;
+  const int my_row = iw0 + lrow;
+  const bool row_ok = wave_active && my_row < n;
+  const int ntiles = (i1 - 1) / IBN + 1;
+  const float c2 = a.scale_log2;
+
+  for (int x = threadIdx.x; x < INW * kMaxBlocks; x += INW * 64) (&s_part[0][0])[x] = 0.0f;
+
+  const int64_t q_stride = int64_t(a.hq) * D;     // elements between consecutive tokens
+  const int64_t kv_stride = int64_t(a.hkv) * D;
+
+  auto load_tiles = [&](int b, int it) {
+    const int j0 = it * IBN;
+    const bf16* kg = static_cast<const bf16*>(a.k) + (int64_t(b) * n * a.hkv + g) * D;
+    const bf16* vg = static_cast<const bf16*>(a.v) + (int64_t(b) * n * a.hkv + g) * D;
+    bf16x8 kr[LPT], vr[LPT];
+#pragma unroll
+    for (int x = 0; x < LPT; ++x) {
+      const int c = threadIdx.x + x * INW * 64;
+      const int r = c / CPR, cc = c % CPR;
+      const int j = j0 + r;
+      if (j < n) {
+        kr[x] = *reinterpret_cast<const bf16x8*>(kg + int64_t(j) * kv_stride + cc * 8);
+        vr[x] = *reinterpret_cast<const bf16x8*>(vg + int64_t(j) * kv_stride + cc * 8);
+      } else {
+        kr[x] = bf16x8{};
+        vr[x] = bf16x8{};
+      }
+    }
+    __syncthreads();                              // the previous tile is no longer read
+#pragma unroll
+    for (int x = 0; x < LPT; ++x) {
+      const int c = threadIdx.x + x * INW * 64;
+      const int r = c / CPR, cc = c % CPR;
+      *reinterpret_cast<bf16x8*>(sK + r * RS + cc * 16) = kr[x];
+      *reinterpret_cast<bf16x8*>(sV + r * RS + cc * 16) = vr[x];
+    }
+    __syncthreads();
+  };
+
+  // S^T and dP^T of one 64-key tile (two 32-key halves), from LDS.
+  auto products = [&](const bf16x8* qf, const bf16x8* df, f32x16* sacc, f32x16* dacc) {
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub) {
+      sacc[sub] = f32x16{};
+      dacc[sub] = f32x16{};
+      const char* kb = sK + (sub * 32 + lrow) * RS + 16 * half;
+      const char* vb = sV + (sub * 32 + lrow) * RS + 16 * half;
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) {
+        sacc[sub] = mma32(*reinterpret_cast<const bf16x8*>(kb + 32 * kk), qf[kk], sacc[sub]);
+        dacc[sub] = mma32(*reinterpret_cast<const bf16x8*>(vb + 32 * kk), df[kk], dacc[sub]);
+      }
+    }
+  };
+  // Key of register r of half-tile `sub` held by this lane.
+  auto key_of = [&](int j0, int sub, int r) { return j0 + sub * 32 + (r >> 2) * 8 + half * 4 + (r & 3); };
+
+  for (int b = 0; b < a.batch; ++b) {
+    bf16x8 qf[KS], df[KS];
+    if (row_ok) {
+      const bf16* qr = static_cast<const bf16*>(a.q) + (int64_t(b) * n + my_row) * q_stride + h * D + 8 * half;
+      const bf16* dr = static_cast<const bf16*>(a.dout) + (int64_t(b) * n + my_row) * q_stride + h * D + 8 * half;
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) {
+        qf[kk] = *reinterpret_cast<const bf16x8*>(qr + 16 * kk);
+        df[kk] = *reinterpret_cast<const bf16x8*>(dr + 16 * kk);
+      }
+    } else {
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) {
+        qf[kk] = bf16x8{};
+        df[kk] = bf16x8{};
+      }
+    }
+
+    // Pass 1: row max, row sum and sum of e * dP (log2 domain for the max).
+    float m = kNegBig, l = 0.0f, u = 0.0f;
+    for (int it = 0; it < ntiles; ++it) {
+      load_tiles(b, it);
+      const int j0 = it * IBN;
+      if (!wave_active || j0 > iw_last) continue;
+      f32x16 sacc[2], dacc[2];
+      products(qf, df, sacc, dacc);
+      float tmax = -INFINITY;
+#pragma unroll
+      for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const bool vis = row_ok && key_of(j0, sub, r) <= my_row;
+          sacc[sub][r] = vis ? sacc[sub][r] * c2 : -INFINITY;
+          tmax = fmaxf(tmax, sacc[sub][r]);
+        }
+      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+      const float m_new = fmaxf(m, tmax);
+      const float alpha = fast_exp2(m - m_new);
+      l *= alpha;
+      u *= alpha;
+#pragma unroll
+      for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float e = fast_exp2(sacc[sub][r] - m_new);
+          l += e;
+          u += e * dacc[sub][r];
+        }
+      m = m_new;
+    }
+    l += __shfl_xor(l, 32, 64);
+    u += __shfl_xor(u, 32, 64);
+    const float lse2 = m + __log2f(l);
+    const float drow = u / l;
+
+    // Pass 2: influence, summed per (row block, key block).
+    for (int it = 0; it < ntiles; ++it) {
+      load_tiles(b, it);
+      const int j0 = it * IBN;
+      if (!wave_active || j0 > iw_last) continue;
+      f32x16 sacc[2], dacc[2];
+      products(qf, df, sacc, dacc);
+      float esum = 0.0f;
+#pragma unroll
+      for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const bool vis = row_ok && key_of(j0, sub, r) <= my_row;
+          const float p = fast_exp2(__builtin_fmaf(sacc[sub][r], c2, -lse2));
+          const float rest = 1.0f - p;
+          const float e = -p * __builtin_amdgcn_rcpf(rest) * (dacc[sub][r] - drow);
+          esum += (vis && rest > 0.0f) ? e : 0.0f;
+        }
+      esum = wave_sum(esum);
+      if (lane == 0) s_part[wave][it] += esum;
+    }
+  }
+  __syncthreads();
+
+  // Block means of the (up to) two 64-row blocks of this tile; blocks above
+  // the diagonal are 0.
+  const int nb = a.nb;
+  for (int x = threadIdx.x; x < 2 * nb; x += INW * 64) {
+    const int ib = x / nb, jb = x - ib * nb;
+    const int I = 2 * t + ib;
+    if (I * IBN >= n) continue;
+    float val = 0.0f;
+    if (jb <= I) {
+      const int rows = min(IBN, n - I * IBN), cols = min(IBN, n - jb * IBN);
+      val = (s_part[2 * ib][jb] + s_part[2 * ib + 1][jb]) / (float(a.batch) * float(rows) * float(cols));
+    }
+    a.ebar[(int64_t(h) * nb + I) * nb + jb] = val;
+  }
+}
+
+}  // namespace
+
+int launch_influence(const InfluenceArgs& a, int head_dim, void* stream) {
+  InfluenceArgs copy = a;
+  void* args[] = {&copy};
+  const void* kernel;
+  if (head_dim == 128) kernel = reinterpret_cast<const void*>(&influence_kernel<128>);
+  else if (head_dim == 64) kernel = reinterpret_cast<const void*>(&influence_kernel<64>);
+  else return static_cast<int>(hipErrorInvalidValue);
+  const unsigned blocks = static_cast<unsigned>(a.hq) * static_cast<unsigned>(a.n_tiles);
+  return static_cast<int>(hipLaunchKernel(kernel, dim3(blocks), dim3(INW * 64), args, 0,
+                                          static_cast<hipStream_t>(stream)));
+}
+
+}  // namespace moa

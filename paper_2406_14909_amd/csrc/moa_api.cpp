@@ -348,4 +348,45 @@ moa_status_t moa_decode_ragged(const moa_plan_t* plan, const void* q, const void
   return ok();
 }
 
+moa_status_t moa_influence(const moa_desc_t* desc, const void* q, const void* k, const void* v,
+                           const void* dout, float* ebar, int32_t batch, int64_t n, void* hip_stream) {
+  if (!desc || !q || !k || !v || !dout || !ebar) return fail(MOA_ERR_INVALID_ARG, "moa_influence: null pointer");
+  const moa_desc_t& d = *desc;
+  if (d.num_kv_heads < 1 || d.num_kv_heads > MOA_MAX_KV_HEADS || d.num_q_heads < 1 ||
+      d.num_q_heads > MOA_MAX_Q_HEADS || d.num_q_heads % d.num_kv_heads != 0)
+    return fail(MOA_ERR_INVALID_ARG, "moa_influence: bad head counts");
+  if (d.head_dim != 64 && d.head_dim != 128)
+    return fail(MOA_ERR_UNSUPPORTED, "moa_influence: head_dim must be 64 or 128");
+  if (d.dtype != MOA_BF16) return fail(MOA_ERR_UNSUPPORTED, "moa_influence: dtype must be MOA_BF16");
+  if (!isfinite(d.softmax_scale) || d.softmax_scale < 0.0f)
+    return fail(MOA_ERR_INVALID_ARG, "moa_influence: softmax_scale must be finite and >= 0");
+  if (batch < 1 || n < 1) return fail(MOA_ERR_INVALID_ARG, "moa_influence: batch and n must be >= 1");
+  if (n > kMaxInfluenceN) return fail(MOA_ERR_UNSUPPORTED, "moa_influence: n must be <= 65536");
+  if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(dout) ||
+      (reinterpret_cast<uintptr_t>(ebar) & 3u))
+    return fail(MOA_ERR_INVALID_ARG, "moa_influence: misaligned pointer");
+  const int64_t nb = (n + kInfluenceBlock - 1) / kInfluenceBlock;
+  const size_t ebar_bytes = sizeof(float) * static_cast<size_t>(d.num_q_heads) * nb * nb;
+  const size_t qb = 2 * static_cast<size_t>(batch) * n * d.num_q_heads * d.head_dim;
+  const size_t kb = 2 * static_cast<size_t>(batch) * n * d.num_kv_heads * d.head_dim;
+  if (overlaps(ebar, ebar_bytes, q, qb) || overlaps(ebar, ebar_bytes, k, kb) || overlaps(ebar, ebar_bytes, v, kb) ||
+      overlaps(ebar, ebar_bytes, dout, qb))
+    return fail(MOA_ERR_INVALID_ARG, "moa_influence: ebar overlaps an input");
+  InfluenceArgs a;
+  memset(&a, 0, sizeof(a));
+  a.q = q; a.k = k; a.v = v; a.dout = dout; a.ebar = ebar;
+  a.n = static_cast<int32_t>(n);
+  a.batch = batch;
+  a.hq = d.num_q_heads;
+  a.hkv = d.num_kv_heads;
+  a.group = d.num_q_heads / d.num_kv_heads;
+  a.n_tiles = static_cast<int32_t>((n + 127) / 128);
+  a.nb = static_cast<int32_t>(nb);
+  const float scale = d.softmax_scale > 0.0f ? d.softmax_scale : static_cast<float>(1.0 / sqrt(double(d.head_dim)));
+  a.scale_log2 = scale * 1.4426950408889634f;
+  const int err = launch_influence(a, d.head_dim, hip_stream);
+  if (err) return fail(MOA_ERR_HIP, "moa_influence: kernel launch failed (hipError " + std::to_string(err) + ")");
+  return ok();
+}
+
 }  // extern "C"

@@ -98,10 +98,28 @@ struct DecodeArgs {
   int64_t offset[MOA_MAX_KV_HEADS];
 };
 
+// Attention-influence profile of dense causal attention (one launch).
+struct InfluenceArgs {
+  const void* q;             // [batch, n, hq, D]
+  const void* k;             // [batch, n, hkv, D]
+  const void* v;             // [batch, n, hkv, D]
+  const void* dout;          // [batch, n, hq, D]
+  float* ebar;               // [hq, nb, nb]
+  int32_t n;
+  int32_t batch;
+  int32_t hq;
+  int32_t hkv;
+  int32_t group;
+  int32_t n_tiles;           // ceil(n / 128) query-row tiles per head
+  int32_t nb;                // ceil(n / 64) blocks
+  float scale_log2;          // softmax scale * log2(e)
+};
+
 // Kernel launchers (return hipError_t as int; 0 = success).
 int launch_prefill(const PrefillArgs& a, int dtype, int head_dim, void* stream);
 int launch_kv_append(const AppendArgs& a, int dtype, int head_dim, void* stream);
 int launch_decode(DecodeArgs a, int dtype, int head_dim, int group, void* stream);
+int launch_influence(const InfluenceArgs& a, int head_dim, void* stream);
 
 constexpr int kPrefillRows = 128;   // query rows per prefill work-group
 constexpr int kPrefillChunk = 16;   // minimum query tiles per prefill dispatch unit
@@ -110,5 +128,7 @@ constexpr int kNumXcd = 8;          // accelerator dies; work-groups go round-ro
 constexpr int kMaxDecodeWorkers = 8192;  // decode workers (waves) per launch, at most
 constexpr int kDecodeMinKeys = 256;      // virtual keys per decode worker, at least
 constexpr int kDecodePartPad = 4;        // partial row: head_dim sums, m, l, 2 pad floats
+constexpr int kInfluenceBlock = 64;      // profiling block (tokens)
+constexpr int kMaxInfluenceN = 65536;    // longest profiled sequence (block sums stay in LDS)
 
 }  // namespace moa

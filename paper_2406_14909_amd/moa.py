@@ -24,7 +24,7 @@ MOA_MAX_Q_HEADS = 512
 EXPORTED = (
     "moa_plan", "moa_plan_tables", "moa_plan_free", "moa_prefill", "moa_kv_append",
     "moa_decode_workspace_bytes", "moa_decode", "moa_last_error", "moa_kv_append_ragged",
-    "moa_decode_ragged",
+    "moa_decode_ragged", "moa_influence",
 )
 
 
@@ -88,6 +88,8 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.moa_kv_append_ragged.restype = ctypes.c_int
     lib.moa_decode_ragged.argtypes = [vp, vp, vp, vp, vp, vp, i32, vp, ctypes.c_size_t, vp]
     lib.moa_decode_ragged.restype = ctypes.c_int
+    lib.moa_influence.argtypes = [ctypes.POINTER(moa_desc_t), vp, vp, vp, vp, vp, i32, i64, vp]
+    lib.moa_influence.restype = ctypes.c_int
     lib.moa_last_error.argtypes = []
     lib.moa_last_error.restype = ctypes.c_char_p
     _lib = lib
@@ -304,3 +306,24 @@ def moa_decode_ragged(plan: Plan, q, k_cache, v_cache, positions, workspace, o=N
                                             v_cache.data_ptr(), o.data_ptr(), positions.data_ptr(), bsz,
                                             workspace.data_ptr(), nbytes, _stream(q, stream)))
     return o
+
+
+def moa_influence(q, k, v, dout, ebar=None, softmax_scale: float = 0.0, stream=None):
+    """Block-averaged attention influence [H_q, nb, nb] (fp32) of dense causal
+    attention over a batch of calibration items (paper Sec. 3.3, Eq. 3).
+
+    q, dout: [B, n, H_q, D] bf16; k, v: [B, n, H_kv, D] bf16 (GPU, contiguous)."""
+    import torch
+    bsz, n, hq, d = (int(x) for x in q.shape)
+    hkv = int(k.shape[2])
+    for t, name, shape in ((q, "q", (bsz, n, hq, d)), (k, "k", (bsz, n, hkv, d)), (v, "v", (bsz, n, hkv, d)),
+                           (dout, "dout", (bsz, n, hq, d))):
+        _need(t, shape, torch.bfloat16, name)
+    nb = -(-n // 64)
+    if ebar is None:
+        ebar = torch.empty((hq, nb, nb), dtype=torch.float32, device=q.device)
+    _need(ebar, (hq, nb, nb), torch.float32, "ebar")
+    desc = moa_desc_t(hq, hkv, d, 0, n, MOA_BF16, float(softmax_scale), 0, 0)
+    _check(load_library().moa_influence(ctypes.byref(desc), q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                                        dout.data_ptr(), ebar.data_ptr(), bsz, n, _stream(q, stream)))
+    return ebar

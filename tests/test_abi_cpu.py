@@ -223,3 +223,21 @@ def test_ragged_entry_points_validate_before_launch():
     assert lib.moa_decode_ragged(h, fake, fake, fake, fake, None, 2, fake, need, None) == M.MOA_ERR_INVALID_ARG
     assert lib.moa_decode_ragged(h, fake, fake, fake, fake, fake, 2, fake, need - 1, None) == M.MOA_ERR_WORKSPACE
     assert lib.moa_decode_ragged(h, fake, fake, fake, fake, fake, 0, fake, need, None) == M.MOA_ERR_INVALID_ARG
+
+
+def test_influence_validates_before_launch():
+    fake = 1 << 20
+    def call(desc=None, q=fake, ebar=fake, batch=1, n=128):
+        d = desc or M.moa_desc_t(4, 2, 128, 0, 0, M.MOA_BF16, 0.0, 0, 0)
+        return lib.moa_influence(ctypes.byref(d), q, fake, fake, fake, ebar, batch, n, None)
+    assert call(q=None) == M.MOA_ERR_INVALID_ARG
+    assert call(desc=M.moa_desc_t(4, 2, 128, 0, 0, M.MOA_F32, 0.0, 0, 0)) == M.MOA_ERR_UNSUPPORTED
+    assert call(desc=M.moa_desc_t(4, 2, 96, 0, 0, M.MOA_BF16, 0.0, 0, 0)) == M.MOA_ERR_UNSUPPORTED
+    assert call(desc=M.moa_desc_t(5, 2, 128, 0, 0, M.MOA_BF16, 0.0, 0, 0)) == M.MOA_ERR_INVALID_ARG
+    assert call(n=65537) == M.MOA_ERR_UNSUPPORTED
+    assert call(n=0) == M.MOA_ERR_INVALID_ARG
+    assert call(batch=0) == M.MOA_ERR_INVALID_ARG
+    assert call(q=fake + 8) == M.MOA_ERR_INVALID_ARG
+    assert call(ebar=fake + 2) == M.MOA_ERR_INVALID_ARG
+    assert "moa_influence" in lib.moa_last_error().decode()
+

@@ -154,3 +154,15 @@ def test_planted_influence_mistakes_are_caught():
     ]
     for m in mutants:
         assert not ok(m)
+
+
+def test_sampled_rows_equal_the_full_oracle():
+    bsz, n, hq, hkv, d = 2, 70, 4, 2, 8
+    q, k, v, do = (_rand(sh, 60 + i) for i, sh in enumerate([(bsz, n, hq, d), (bsz, n, hkv, d),
+                                                              (bsz, n, hkv, d), (bsz, n, hq, d)]))
+    full = io.influence_ref(io.causal_probabilities(q, k), io.grad_wrt_probabilities(v, do, hq))
+    rows = [0, 1, 33, 64, 69]
+    for b, h in ((0, 0), (1, 3)):
+        np.testing.assert_allclose(io.influence_rows_ref(q, k, v, do, b, h, rows), full[b, h, rows],
+                                   rtol=0, atol=1e-13)
+
