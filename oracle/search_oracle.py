@@ -1,0 +1,92 @@
+"""Plain fp64 CPU oracle for the MoA rule search (rule-loss table and selection).
+
+TEST INFRASTRUCTURE ONLY.  Only the test-suite may import this module.  It
+shares no code with the library.
+
+What it computes, in the paper's terms:
+
+* Candidate rules (Appendix "Main Setup"): 6 values of alpha uniformly
+  spaced over [-2048, 8192] and 9 values of beta uniformly spaced over
+  [0, 1], 54 (alpha, beta) pairs per head.
+* Rule loss (Sec. 3.3, Eq. 4): the accuracy loss of giving head h rule r at
+  length N is the sum of the head's average attention influence over the
+  positions the rule masks, Delta L_{h,r} = sum_ij M_{r,ij} E_bar_{h,ij}.
+  E_bar is block-averaged, so every token (i, j) of a block carries the
+  block's value.  M_r marks the causal pairs (j <= i) that the rule's mask
+  hides: the rule's window (and sinks, block band) from the plan's reading.
+* Density of a rule at length N: the fraction of the causal pairs it keeps.
+* Single-length selection (Appendix "Optimizing at Single Length"): choose
+  one rule per head minimising the mean loss subject to the mean density
+  not exceeding the budget; optionally at most K distinct rules per layer.
+  Solved here by enumerating every assignment (tiny head counts only).
+
+Parity status: pinned by the CPU tests (hand-worked masked sums, the
+identity sum_r-independent totals, brute-force enumeration checked against
+a library MILP solver); nothing is unpinned.
+"""
+from __future__ import annotations
+
+import itertools
+from typing import Optional, Sequence
+
+import numpy as np
+
+from .moa_oracle import visible_mask, window_ref
+
+
+def candidate_rules(n_alpha: int = 6, n_beta: int = 9):
+    """The (alpha, beta) grid: alpha uniform over [-2048, 8192], beta over [0, 1]."""
+    alphas = np.linspace(-2048.0, 8192.0, n_alpha)
+    betas = np.linspace(0.0, 1.0, n_beta)
+    pairs = [(float(a), float(b)) for a in alphas for b in betas]
+    return np.array([p[0] for p in pairs]), np.array([p[1] for p in pairs])
+
+
+def masked_pairs(n: int, w: int, s: int, block: int = 0) -> np.ndarray:
+    """Boolean [n, n]: causal pairs hidden by the mask of window w, sinks s."""
+    causal = np.tril(np.ones((n, n), dtype=bool))
+    return causal & ~visible_mask(n, n, w, s, 0, block)
+
+
+def rule_loss_ref(ebar: np.ndarray, n: int, num_sink: int, alpha: Sequence[float], beta: Sequence[float],
+                  span_includes_sinks: bool = False, block: int = 0, profile_block: int = 64):
+    """(Delta L [H, R], density [R]) of every rule for every head at length n.
+
+    ebar: [H, nb, nb] block-averaged influence (profile_block x profile_block
+    blocks); each token pair takes its block's value (Eq. 4 summed token by
+    token)."""
+    ebar = np.asarray(ebar, dtype=np.float64)
+    h = ebar.shape[0]
+    tok = np.repeat(np.repeat(ebar, profile_block, axis=1), profile_block, axis=2)[:, :n, :n]
+    causal_count = n * (n + 1) // 2
+    dl = np.zeros((h, len(alpha)), dtype=np.float64)
+    dens = np.zeros(len(alpha), dtype=np.float64)
+    for r, (a, b) in enumerate(zip(alpha, beta)):
+        w = window_ref(a, b, n, num_sink, span_includes_sinks)
+        m = masked_pairs(n, w, num_sink, block)
+        dl[:, r] = (tok * m[None]).sum(axis=(1, 2))
+        dens[r] = (causal_count - int(m.sum())) / causal_count
+    return dl, dens
+
+
+def select_bruteforce(dl: np.ndarray, density: np.ndarray, budget: float,
+                      layer_of: Optional[Sequence[int]] = None, max_rules_per_layer: int = 0):
+    """Exhaustive single-length selection: argmin mean_h dl[h, r_h] subject to
+    mean_h density[r_h] <= budget (and at most max_rules_per_layer distinct
+    rules among the heads of a layer when given).  Returns (rules, loss) or
+    (None, inf) when no assignment fits."""
+    h, r = dl.shape
+    best, best_rules = np.inf, None
+    for combo in itertools.product(range(r), repeat=h):
+        if np.mean(density[list(combo)]) > budget + 1e-12:
+            continue
+        if max_rules_per_layer and layer_of is not None:
+            per_layer = {}
+            for hh, rr in enumerate(combo):
+                per_layer.setdefault(layer_of[hh], set()).add(rr)
+            if any(len(v) > max_rules_per_layer for v in per_layer.values()):
+                continue
+        loss = float(np.mean([dl[hh, rr] for hh, rr in enumerate(combo)]))
+        if loss < best:
+            best, best_rules = loss, list(combo)
+    return best_rules, best
