@@ -110,6 +110,8 @@ def main() -> int:
                     help="time the attention-influence profile (moa_influence) on the workload's layer shape")
     ap.add_argument("--influence-n", type=int, default=8192, help="profiled length for --influence")
     ap.add_argument("--influence-items", type=int, default=4, help="calibration items for --influence")
+    ap.add_argument("--rule-loss", action="store_true",
+                    help="time the rule-loss table (moa_rule_loss): 54 rules x 1024 heads at --influence-n")
     ap.add_argument("--peaks", action="store_true",
                     help="measure practical ceilings: hipBLASLt bf16 GEMM TFLOP/s and streaming-read GB/s")
     args = ap.parse_args()
@@ -127,6 +129,9 @@ def main() -> int:
         return 0
     if args.influence:
         print(json.dumps(measure_influence(args)), flush=True)
+        return 0
+    if args.rule_loss:
+        print(json.dumps(measure_rule_loss(args)), flush=True)
         return 0
 
     sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
@@ -326,6 +331,45 @@ def measure_influence(args):
                      "achieved": round(flops / (ms / 1e3) / 1e12, 2), "peak": BF16_MFMA_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(flops / (ms / 1e3) / 1e12 / BF16_MFMA_PEAK_TFLOPS, 4),
                      "flops_per_launch": flops},
+    }
+
+
+def measure_rule_loss(args):
+    """Times moa_rule_loss for a 32-layer x 32-head model (1024 profiles) at the
+    profiled length, over the paper's 54-rule grid (block band, span includes
+    sinks).  Algorithmic bytes: the causal half of the fp32 profile read once
+    plus the fp64 table written."""
+    import torch
+
+    sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+    from paper_2406_14909_amd import moa as M
+    from paper_2406_14909_amd import search
+
+    heads, n = 1024, args.influence_n
+    nb = -(-n // 64)
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(21)
+    ebar = torch.randn((heads, nb, nb), generator=gen, device="cuda").tril_()
+    a, b = search.candidate_rules()
+    flags = M.MOA_BLOCK_BAND | M.MOA_SPAN_INCLUDES_SINKS
+    for _ in range(max(1, args.warmup)):
+        M.moa_rule_loss(ebar, n, 64, a, b, flags)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    for _ in range(args.steps):
+        M.moa_rule_loss(ebar, n, 64, a, b, flags)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / args.steps
+    nbytes = heads * (nb * (nb + 1) // 2) * 4 + heads * len(a) * 8
+    return {
+        "metric": "rule-loss table time", "unit": "ms", "value": round(ms, 4), "higher_is_better": False,
+        "config": {"heads": heads, "n": n, "rules": len(a), "flags": "block_band|span_includes_sinks"},
+        "roofline": {"kernel": "rule_loss_kernel", "bound": "hbm", "achieved": round(nbytes / (ms / 1e3) / 1e9, 1),
+                     "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(nbytes / (ms / 1e3) / 1e9 / HBM_PEAK_GBS, 4),
+                     "bytes_per_launch": nbytes},
     }
 
 

@@ -27,6 +27,8 @@
  *   moa_influence  the profiling step that precedes the rule search: the
  *                  block-averaged attention influence of dense attention
  *                  (paper Sec. 3.3, Eq. 3).
+ *   moa_rule_loss  the loss table of candidate rules from that profile
+ *                  (paper Sec. 3.3, Eq. 4), input of the rule selection.
  *
  * Definitions used throughout (s = num_sink, w_g = window of KV head g):
  *   window    w_g = min(max(floor(alpha_g + beta_g * N), 1), N), evaluated
@@ -230,6 +232,23 @@ moa_status_t moa_decode_ragged(const moa_plan_t* plan, const void* q, const void
  * one kernel launch; the result does not depend on the launch order. */
 moa_status_t moa_influence(const moa_desc_t* desc, const void* q, const void* k, const void* v,
                            const void* dout, float* ebar, int32_t batch, int64_t n, void* hip_stream);
+
+/* Rule-loss table (paper Sec. 3.3, Eq. 4): the accuracy loss of giving head h
+ * candidate rule r at length n is its block-averaged influence summed over the
+ * causal pairs the rule masks,
+ *   dl[h][r] = sum over i, j with j <= i of M_r(i, j) * ebar[h][i / 64][j / 64],
+ * M_r(i, j) = 1 iff rule r's mask (window from (alpha[r], beta[r]) at length n
+ * exactly as moa_plan evaluates it under `flags`, num_sink sinks, token or
+ * MOA_BLOCK_BAND band) hides key j from query i.  density[r] = fraction of the
+ * n (n + 1) / 2 causal pairs rule r keeps.
+ * ebar   fp32 device [num_heads, nb, nb], nb = ceil(n / 64) (moa_influence output)
+ * dl     fp64 device [num_heads, num_rules];  density fp64 device [num_rules]
+ * alpha, beta: host arrays of num_rules finite doubles; 1 <= num_rules <= 64;
+ * 1 <= n <= 65536.  fp64 sums (exact masked-pair counts in closed form).
+ * Allocates nothing; one kernel launch. */
+moa_status_t moa_rule_loss(const float* ebar, int32_t num_heads, int64_t n, int32_t num_sink, uint32_t flags,
+                           const double* alpha, const double* beta, int32_t num_rules, double* dl,
+                           double* density, void* hip_stream);
 
 /* Thread-local message of the calling thread's last non-OK status ("" if none). */
 const char* moa_last_error(void);

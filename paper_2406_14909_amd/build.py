@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG_DIR, "_build")
 LIB_PATH = os.path.join(PKG_DIR, "libmoa.so")
 
-HIP_SOURCES = ["kv_append.hip", "decode.hip", "prefill.hip", "influence.hip"]
+HIP_SOURCES = ["kv_append.hip", "decode.hip", "prefill.hip", "influence.hip", "rule_loss.hip"]
 HOST_SOURCES = ["moa_api.cpp"]
 
 ARCH = "gfx950"

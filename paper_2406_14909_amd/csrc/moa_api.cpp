@@ -61,6 +61,26 @@ static moa_status_t decode_args(const moa_plan_s& p, const char* who, const void
   return ok();
 }
 
+// Elastic rule alpha + beta * N (paper Sec. 3.2, Eq. 2), floored.  Default:
+// the value is the band, clipped to [1, N].  MOA_SPAN_INCLUDES_SINKS: it is the
+// whole span S (sinks + band, Appendix "Attention Span"), clipped to [0, N],
+// and the band is S - s, at least 1.
+static int64_t rule_window(double alpha, double beta, int64_t n, int32_t num_sink, uint32_t flags) {
+  const double nd = static_cast<double>(n);
+  volatile double prod = beta * nd;   // separate rounding: no fused multiply-add
+  const double x = alpha + prod;
+  if (flags & MOA_SPAN_INCLUDES_SINKS) {
+    int64_t span;
+    if (!(x >= 0.0)) span = 0;
+    else if (x >= nd) span = n;
+    else span = static_cast<int64_t>(floor(x));
+    return std::max<int64_t>(span - num_sink, 1);
+  }
+  if (!(x >= 1.0)) return 1;
+  if (x >= nd) return n;
+  return static_cast<int64_t>(floor(x));
+}
+
 static bool aligned16(const void* ptr) { return (reinterpret_cast<uintptr_t>(ptr) & 15u) == 0; }
 
 static bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
@@ -117,26 +137,8 @@ moa_status_t moa_plan(const moa_desc_t* desc, const double* alpha, const double*
   p->window.resize(hkv);
   p->capacity.resize(hkv);
   p->offset.assign(hkv + 1, 0);
-  const double nd = static_cast<double>(d.n);
   for (int h = 0; h < hkv; ++h) {
-    // Elastic rule alpha + beta * N (paper Sec. 3.2, Eq. 2), floored.  Default:
-    // the value is the band, clipped to [1, N].  MOA_SPAN_INCLUDES_SINKS: it is
-    // the whole span S (sinks + band, Appendix "Attention Span"), clipped to
-    // [0, N], and the band is S - s, at least 1.
-    volatile double prod = beta[h] * nd;   // separate rounding: no fused multiply-add
-    const double x = alpha[h] + prod;
-    int64_t w;
-    if (d.flags & MOA_SPAN_INCLUDES_SINKS) {
-      int64_t span;
-      if (!(x >= 0.0)) span = 0;
-      else if (x >= nd) span = d.n;
-      else span = static_cast<int64_t>(floor(x));
-      w = std::max<int64_t>(span - d.num_sink, 1);
-    } else {
-      if (!(x >= 1.0)) w = 1;
-      else if (x >= nd) w = d.n;
-      else w = static_cast<int64_t>(floor(x));
-    }
+    const int64_t w = rule_window(alpha[h], beta[h], d.n, d.num_sink, d.flags);
     p->window[h] = static_cast<int32_t>(w);
     p->capacity[h] = static_cast<int32_t>(w + d.num_sink);
     p->offset[h + 1] = p->offset[h] + p->capacity[h];
@@ -386,6 +388,46 @@ moa_status_t moa_influence(const moa_desc_t* desc, const void* q, const void* k,
   a.scale_log2 = scale * 1.4426950408889634f;
   const int err = launch_influence(a, d.head_dim, hip_stream);
   if (err) return fail(MOA_ERR_HIP, "moa_influence: kernel launch failed (hipError " + std::to_string(err) + ")");
+  return ok();
+}
+
+moa_status_t moa_rule_loss(const float* ebar, int32_t num_heads, int64_t n, int32_t num_sink, uint32_t flags,
+                           const double* alpha, const double* beta, int32_t num_rules, double* dl,
+                           double* density, void* hip_stream) {
+  if (!ebar || !alpha || !beta || !dl || !density) return fail(MOA_ERR_INVALID_ARG, "moa_rule_loss: null pointer");
+  if (num_heads < 1 || num_rules < 1 || num_rules > kMaxRules)
+    return fail(MOA_ERR_INVALID_ARG, "moa_rule_loss: need num_heads >= 1 and 1 <= num_rules <= 64");
+  if (n < 1 || n > kMaxInfluenceN) return fail(MOA_ERR_INVALID_ARG, "moa_rule_loss: n must be in [1, 65536]");
+  if (num_sink < 0 || num_sink >= (1 << 30)) return fail(MOA_ERR_INVALID_ARG, "moa_rule_loss: bad num_sink");
+  if ((flags & ~(MOA_SPAN_INCLUDES_SINKS | MOA_BLOCK_BAND)) != 0)
+    return fail(MOA_ERR_INVALID_ARG, "moa_rule_loss: unknown flags");
+  if ((reinterpret_cast<uintptr_t>(ebar) & 3u) || (reinterpret_cast<uintptr_t>(dl) & 7u) ||
+      (reinterpret_cast<uintptr_t>(density) & 7u))
+    return fail(MOA_ERR_INVALID_ARG, "moa_rule_loss: misaligned pointer");
+  for (int r = 0; r < num_rules; ++r)
+    if (!isfinite(alpha[r]) || !isfinite(beta[r]))
+      return fail(MOA_ERR_INVALID_ARG, "moa_rule_loss: alpha and beta must be finite");
+  const int64_t nb = (n + kInfluenceBlock - 1) / kInfluenceBlock;
+  const size_t ebar_bytes = sizeof(float) * static_cast<size_t>(num_heads) * nb * nb;
+  const size_t dl_bytes = sizeof(double) * static_cast<size_t>(num_heads) * num_rules;
+  if (overlaps(dl, dl_bytes, ebar, ebar_bytes) || overlaps(density, sizeof(double) * num_rules, ebar, ebar_bytes) ||
+      overlaps(density, sizeof(double) * num_rules, dl, dl_bytes))
+    return fail(MOA_ERR_INVALID_ARG, "moa_rule_loss: output overlaps another buffer");
+  RuleLossArgs a;
+  memset(&a, 0, sizeof(a));
+  a.ebar = ebar; a.dl = dl; a.density = density;
+  a.num_heads = num_heads;
+  a.n = static_cast<int32_t>(n);
+  a.nb = static_cast<int32_t>(nb);
+  a.num_rules = num_rules;
+  a.num_sink = num_sink;
+  a.band_shift = (flags & MOA_BLOCK_BAND) ? 6 : 0;
+  for (int r = 0; r < num_rules; ++r) {
+    const int64_t w = rule_window(alpha[r], beta[r], n, num_sink, flags);
+    a.window[r] = static_cast<int32_t>((flags & MOA_BLOCK_BAND) ? (w + MOA_BAND_BLOCK - 1) / MOA_BAND_BLOCK : w);
+  }
+  const int err = launch_rule_loss(a, hip_stream);
+  if (err) return fail(MOA_ERR_HIP, "moa_rule_loss: kernel launch failed (hipError " + std::to_string(err) + ")");
   return ok();
 }
 

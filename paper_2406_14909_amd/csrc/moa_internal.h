@@ -115,11 +115,27 @@ struct InfluenceArgs {
   float scale_log2;          // softmax scale * log2(e)
 };
 
+// Rule-loss table of a set of candidate rules (one launch).
+constexpr int kMaxRules = 64;
+struct RuleLossArgs {
+  const float* ebar;         // [num_heads, nb, nb] block-averaged influence
+  double* dl;                // [num_heads, num_rules]
+  double* density;           // [num_rules]
+  int32_t num_heads;
+  int32_t n;
+  int32_t nb;
+  int32_t num_rules;
+  int32_t num_sink;
+  int32_t band_shift;        // 0: token band; 6: band in 64-token blocks
+  int32_t window[kMaxRules]; // per rule: band length in units of 2^band_shift tokens
+};
+
 // Kernel launchers (return hipError_t as int; 0 = success).
 int launch_prefill(const PrefillArgs& a, int dtype, int head_dim, void* stream);
 int launch_kv_append(const AppendArgs& a, int dtype, int head_dim, void* stream);
 int launch_decode(DecodeArgs a, int dtype, int head_dim, int group, void* stream);
 int launch_influence(const InfluenceArgs& a, int head_dim, void* stream);
+int launch_rule_loss(const RuleLossArgs& a, void* stream);
 
 constexpr int kPrefillRows = 128;   // query rows per prefill work-group
 constexpr int kPrefillChunk = 16;   // minimum query tiles per prefill dispatch unit

@@ -24,7 +24,7 @@ MOA_MAX_Q_HEADS = 512
 EXPORTED = (
     "moa_plan", "moa_plan_tables", "moa_plan_free", "moa_prefill", "moa_kv_append",
     "moa_decode_workspace_bytes", "moa_decode", "moa_last_error", "moa_kv_append_ragged",
-    "moa_decode_ragged", "moa_influence",
+    "moa_decode_ragged", "moa_influence", "moa_rule_loss",
 )
 
 
@@ -90,6 +90,9 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.moa_decode_ragged.restype = ctypes.c_int
     lib.moa_influence.argtypes = [ctypes.POINTER(moa_desc_t), vp, vp, vp, vp, vp, i32, i64, vp]
     lib.moa_influence.restype = ctypes.c_int
+    lib.moa_rule_loss.argtypes = [vp, i32, i64, i32, ctypes.c_uint32, ctypes.POINTER(ctypes.c_double),
+                                  ctypes.POINTER(ctypes.c_double), i32, vp, vp, vp]
+    lib.moa_rule_loss.restype = ctypes.c_int
     lib.moa_last_error.argtypes = []
     lib.moa_last_error.restype = ctypes.c_char_p
     _lib = lib
@@ -327,3 +330,26 @@ def moa_influence(q, k, v, dout, ebar=None, softmax_scale: float = 0.0, stream=N
     _check(load_library().moa_influence(ctypes.byref(desc), q.data_ptr(), k.data_ptr(), v.data_ptr(),
                                         dout.data_ptr(), ebar.data_ptr(), bsz, n, _stream(q, stream)))
     return ebar
+
+
+def moa_rule_loss(ebar, n: int, num_sink: int, alpha, beta, flags: int = 0, stream=None):
+    """(dl [H, R] fp64, density [R] fp64) on the GPU: the loss of every candidate
+    rule for every head at length n (paper Sec. 3.3, Eq. 4) from the
+    block-averaged influence ebar [H, nb, nb] (fp32, GPU)."""
+    import torch
+    h = int(ebar.shape[0])
+    nb = -(-int(n) // 64)
+    _need(ebar, (h, nb, nb), torch.float32, "ebar")
+    a = np.ascontiguousarray(alpha, dtype=np.float64)
+    b = np.ascontiguousarray(beta, dtype=np.float64)
+    if a.shape != b.shape or a.ndim != 1:
+        raise MoaError(MOA_ERR_INVALID_ARG, "alpha and beta must be 1-D arrays of the same length")
+    r = int(a.shape[0])
+    dl = torch.empty((h, r), dtype=torch.float64, device=ebar.device)
+    dens = torch.empty((r,), dtype=torch.float64, device=ebar.device)
+    _check(load_library().moa_rule_loss(ebar.data_ptr(), h, int(n), int(num_sink), int(flags),
+                                        a.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
+                                        b.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), r,
+                                        dl.data_ptr(), dens.data_ptr(), _stream(ebar, stream)))
+    return dl, dens
+

@@ -1,0 +1,111 @@
+"""GPU parity of the rule-loss table (paper Sec. 3.3, Eq. 4) and the whole
+profile -> loss -> selection -> plan loop, against the fp64 oracle chain.
+
+The table sums fp32 block means with exact integer pair counts in fp64 on both
+sides, in different orders: relative agreement ~1e-12 is expected, 1e-9 is
+required (a bound far below the gaps that decide the selection)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import workloads
+from oracle import influence_oracle as io
+from paper_2406_14909_amd import moa as M
+from paper_2406_14909_amd import search
+
+pytestmark = pytest.mark.gpu
+
+
+def _say(*a):
+    print("[case]", *a, flush=True)
+
+
+def _ebar(h, n, seed):
+    nb = -(-n // 64)
+    rng = np.random.default_rng(seed)
+    return np.tril(rng.normal(size=(h, nb, nb))).astype(np.float32)
+
+
+RULE_CASES = [
+    # H, n, sinks, flags
+    (4, 64, 0, 0),
+    (3, 100, 5, 0),
+    (5, 1000, 64, M.MOA_SPAN_INCLUDES_SINKS),
+    (2, 2048, 64, M.MOA_SPAN_INCLUDES_SINKS | M.MOA_BLOCK_BAND),
+    (2, 777, 3, M.MOA_BLOCK_BAND),
+]
+
+
+@pytest.mark.parametrize("case", RULE_CASES, ids=lambda c: f"H{c[0]}-n{c[1]}-s{c[2]}-f{c[3]}")
+def test_rule_loss_matches_oracle(case):
+    h, n, s, flags = case
+    _say("rule loss", case)
+    e = _ebar(h, n, 600 + n)
+    a, b = search.candidate_rules()
+    a = a * (n / 8192.0)          # scale the grid to the length so rules differ
+    dl, dens = M.moa_rule_loss(torch.from_numpy(e).cuda(), n, s, a, b, flags)
+    torch.cuda.synchronize()
+    ref_dl, ref_dens = oracle.rule_loss_ref(e, n, s, a, b, span_includes_sinks=bool(flags & M.MOA_SPAN_INCLUDES_SINKS),
+                                            block=64 if flags & M.MOA_BLOCK_BAND else 0)
+    np.testing.assert_allclose(dens.cpu().numpy(), ref_dens, rtol=0, atol=1e-15)
+    scale = np.abs(ref_dl).max() + 1e-30
+    np.testing.assert_allclose(dl.cpu().numpy(), ref_dl, rtol=0, atol=1e-9 * scale)
+
+
+def test_rule_loss_full_size_sampled_rules():
+    """1024 heads (a 32-layer, 32-head model) at the paper's 8192-token profile
+    length, paper grid, block band and span-includes-sinks; six rules checked."""
+    h, n, s = 1024, 8192, 64
+    _say("rule loss", f"H={h} n={n}")
+    flags = M.MOA_SPAN_INCLUDES_SINKS | M.MOA_BLOCK_BAND
+    e = _ebar(h, n, 700)
+    a, b = search.candidate_rules()
+    dl, dens = M.moa_rule_loss(torch.from_numpy(e).cuda(), n, s, a, b, flags)
+    torch.cuda.synchronize()
+    dl, dens = dl.cpu().numpy(), dens.cpu().numpy()
+    for r in (0, 9, 20, 31, 44, 53):
+        heads = [0, 511, 1023]
+        ref_dl, ref_dens = oracle.rule_loss_ref(e[heads], n, s, a[r:r + 1], b[r:r + 1], span_includes_sinks=True, block=64)
+        assert dens[r] == pytest.approx(ref_dens[0], abs=1e-15)
+        np.testing.assert_allclose(dl[heads, r], ref_dl[:, 0], rtol=0, atol=1e-9 * (np.abs(ref_dl).max() + 1e-30))
+
+
+def test_profile_loss_select_plan_loop():
+    """Influence (GPU) -> rule losses (GPU) -> selection -> plan -> decode, and
+    the same chain in the oracle: equal optimal loss, a feasible selection."""
+    bsz, n, h, d, s = 2, 512, 3, 128, 64
+    _say("search loop", f"B={bsz} n={n} H={h}")
+    q = workloads.randn((bsz, n, h, d), 800, torch.bfloat16, "cuda")
+    k = workloads.randn((bsz, n, h, d), 801, torch.bfloat16, "cuda")
+    v = workloads.randn((bsz, n, h, d), 802, torch.bfloat16, "cuda")
+    do = workloads.randn((bsz, n, h, d), 803, torch.bfloat16, "cuda")
+    a, b = search.candidate_rules()
+    a = a / 16.0                 # rules that differ at this short length
+    flags = M.MOA_SPAN_INCLUDES_SINKS | M.MOA_BLOCK_BAND
+    ebar = M.moa_influence(q, k, v, do)
+    dl, dens = M.moa_rule_loss(ebar, n, s, a, b, flags)
+    torch.cuda.synchronize()
+    dl, dens = dl.cpu().numpy(), dens.cpu().numpy()
+    budget = 0.5
+    rules, loss = search.select_rules(dl, dens, budget)
+
+    ref_e = io.influence_profile_ref(q, k, v, do)
+    ref_dl, ref_dens = oracle.rule_loss_ref(ref_e, n, s, a, b, span_includes_sinks=True, block=64)
+    ref_rules, ref_loss = oracle.select_bruteforce(ref_dl, ref_dens, budget)
+    assert rules is not None and ref_rules is not None
+    assert np.mean(ref_dens[rules]) <= budget + 1e-12            # the selection is feasible
+    # its loss under the oracle's table is optimal up to the profile's error
+    tol = 1e-3 * np.abs(ref_dl).max()
+    assert float(np.mean(ref_dl[np.arange(h), rules])) <= ref_loss + tol
+    assert loss == pytest.approx(ref_loss, abs=tol)
+    # the chosen rules make a working plan
+    plan = M.moa_plan(h, h, d, s, n, "bf16", a[rules], b[rules], flags=flags)
+    assert np.array_equal(plan.window, oracle.plan_ref(a[rules], b[rules], n, s, span_includes_sinks=True)["window"])
+    kc, vc, pos = M.new_cache(plan, bsz)
+    ws = M.new_workspace(plan, bsz)
+    M.moa_kv_append(plan, kc, vc, pos, k, v, 0)
+    od = M.moa_decode(plan, q[:, n - 1].contiguous(), kc, vc, n - 1, ws)
+    torch.cuda.synchronize()
+    ref = oracle.decode_ref(q[:, n - 1], k, v, plan.window, s)
+    assert np.abs(od.float().cpu().numpy() - ref).max() <= 1e-2
