@@ -22,7 +22,6 @@ moa_status_t fail(moa_status_t st, const std::string& msg) {
 
 moa_status_t ok() { return MOA_OK; }
 
-static int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 // Workspace: decode partials, fp32 [workers + batch * hkv][group][head_dim + 4]
 // (acc[head_dim], running max m, running sum l, padding), for the largest
