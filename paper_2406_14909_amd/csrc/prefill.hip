@@ -191,19 +191,9 @@ __global__ void __launch_bounds__(NW * 64, 2) prefill_kernel(PrefillArgs a) {
   const char* kg = static_cast<const char*>(a.k) + (int64_t(b) * n * a.hkv + g) * RB;
   const char* vg = static_cast<const char*>(a.v) + (int64_t(b) * n * a.hkv + g) * RB;
 
-  // Q^T fragments of this lane's query row (zeros past the end).
+  // Q^T fragments of this lane's query row (loaded after the first tiles' DMA
+  // is issued, see the pipeline prologue).
   typename M::frag qf[KS];
-  {
-    const int i = iw0 + lrow;
-    if (wave_active && i < i1) {
-      const T* qrow = qg + int64_t(i) * q_row_stride;
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk) qf[kk] = load_frag(qrow, kk, half);
-    } else {
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk) qf[kk] = typename M::frag{};
-    }
-  }
 
   // Direct-to-LDS tile loads: DMA instruction I writes buffer bytes
   // [I*1024, I*1024 + 1024) and lane L's 16 bytes land at chunk I*64 + L.
@@ -322,6 +312,22 @@ __global__ void __launch_bounds__(NW * 64, 2) prefill_kernel(PrefillArgs a) {
     issue_k(0);
   }
   if (ntiles > 1) issue_k(1);
+  {
+    const int i = iw0 + lrow;
+    if (wave_active && i < i1) {
+      const T* qrow = qg + int64_t(i) * q_row_stride;
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) qf[kk] = load_frag(qrow, kk, half);
+    } else {
+#pragma unroll
+      for (int kk = 0; kk < KS; ++kk) qf[kk] = typename M::frag{};
+    }
+  }
+  // Wait for Q (and the first tiles) here, once.  The tile DMA is opaque to
+  // the compiler's wait-count tracking, which would otherwise place waits for
+  // the Q loads inside the tile loop, where they would also drain the
+  // prefetches in flight.
+  __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
   for (int it = 0; it < ntiles; ++it) {
     const int j0 = tile_j0(it);
     if constexpr (KST == 3) {
