@@ -376,6 +376,8 @@ def measure_rule_loss(args):
 def measure_peaks():
     """Practical ceilings on this GPU, measured with library kernels.
 
+    HBM read: the package's streaming-read calibration program (16-byte loads
+    over 2 GiB, a sweep of grid sizes and loads in flight), best rate;
     MFMA: a 16384^3 bf16 GEMM (torch.matmul -> hipBLASLt), best of 5.
     HBM read: torch.sum over 8 GiB of bf16 (a streaming reduction), best of 5;
     HBM copy: a 4 GiB device-to-device copy (read + write), best of 5.
@@ -406,7 +408,16 @@ def measure_peaks():
     src = torch.ones((4 << 30) // 2, device="cuda", dtype=torch.bfloat16)
     dst = torch.empty_like(src)
     copy_ms = best_ms(lambda: dst.copy_(src))
+    probe = os.path.join(ROOT, "paper_2406_14909_amd", "_build", "stream_read")
+    stream_best = None
+    if os.path.exists(probe):
+        import subprocess
+        out = subprocess.run([probe], capture_output=True, text=True, timeout=120).stdout
+        log(out.strip())
+        best = [line.split()[1] for line in out.splitlines() if line.startswith("best ")]
+        stream_best = float(best[0]) if best else None
     return {
+        "hip_stream_read_gbs": stream_best,
         "gemm_bf16_16384_tflops": round(2.0 * n ** 3 / (gemm_ms / 1e3) / 1e12, 1),
         "stream_read_gbs": round((8 << 30) / (read_ms / 1e3) / 1e9, 1),
         "copy_read_plus_write_gbs": round(2 * (4 << 30) / (copy_ms / 1e3) / 1e9, 1),
