@@ -19,10 +19,14 @@ What it computes, in the paper's terms:
   one rule per head minimising the mean loss subject to the mean density
   not exceeding the budget; optionally at most K distinct rules per layer.
   Solved here by enumerating every assignment (tiny head counts only).
+* Multi-length search (Sec. 3.4, Appendix "Optimizing at Multiple Lengths"):
+  the Pareto front of the per-length mean losses over all assignments that
+  meet every length's density budget, by enumeration.
 
-Parity status: pinned by the CPU tests (hand-worked masked sums, the
-identity sum_r-independent totals, brute-force enumeration checked against
-a library MILP solver); nothing is unpinned.
+Parity status: pinned by the CPU tests (a hand-worked masked sum, the
+loss / density identity under a unit profile, hand-worked selection and
+Pareto examples, enumeration checked against a library MILP solver);
+nothing is unpinned.
 """
 from __future__ import annotations
 
@@ -90,3 +94,24 @@ def select_bruteforce(dl: np.ndarray, density: np.ndarray, budget: float,
         if loss < best:
             best, best_rules = loss, list(combo)
     return best_rules, best
+
+
+def dominates(p, q) -> bool:
+    """p is no worse than q at every length and better at one."""
+    p, q = np.asarray(p), np.asarray(q)
+    return bool(np.all(p <= q) and np.any(p < q))
+
+
+def pareto_front_bruteforce(dls, densities, budgets):
+    """All non-dominated per-length loss vectors over the feasible assignments
+    (each a tuple of mean losses, one per length), by enumeration."""
+    dls = [np.asarray(d, dtype=np.float64) for d in dls]
+    h, r = dls[0].shape
+    points = set()
+    for combo in itertools.product(range(r), repeat=h):
+        ok = all(np.mean(np.asarray(densities[i])[list(combo)]) <= budgets[i] + 1e-12
+                 for i in range(len(dls)) if budgets[i] is not None)
+        if ok:
+            points.add(tuple(float(np.mean([d[hh, rr] for hh, rr in enumerate(combo)])) for d in dls))
+    return sorted(p for p in points if not any(dominates(q, p) for q in points))
+

@@ -50,3 +50,25 @@ def test_selection_with_layer_limit_matches_exhaustive_search():
 def test_infeasible_budget():
     dl, dens = _table(1)
     assert search.select_rules(dl, dens, float(dens.min()) - 1e-3) == (None, np.inf)
+
+
+@pytest.mark.parametrize("seed", range(3))
+def test_multi_length_front_lies_on_the_exact_front(seed):
+    rng = np.random.default_rng(20 + seed)
+    h, r = 3, 6
+    dls = [rng.normal(size=(h, r)) for _ in range(2)]
+    dens = [rng.uniform(0.2, 1.0, r), rng.uniform(0.2, 1.0, r)]
+    budgets = [0.7, 0.8]
+    val = rng.normal(size=(h, r))
+    front, best = search.select_multi_length(dls, dens, budgets, intervals=5, val_dl=val)
+    exact = oracle.pareto_front_bruteforce(dls, dens, budgets)
+    assert front
+    for rules, vec in front:
+        assert any(np.allclose(vec, p, atol=1e-12) for p in exact)          # every member is Pareto-optimal
+        for i in range(2):
+            assert np.mean(dens[i][rules]) <= budgets[i] + 1e-12
+    for i in range(2):                                                      # both extreme points are found
+        assert min(v[i] for _, v in front) == pytest.approx(min(p[i] for p in exact), abs=1e-12)
+    assert best is not None and float(np.mean(val[np.arange(h), best[0]])) == pytest.approx(
+        min(float(np.mean(val[np.arange(h), f[0]])) for f in front), abs=1e-12)
+

@@ -79,3 +79,16 @@ def test_selection_layer_limit():
     assert rules == [0, 2, 0, 0] and loss == 0.0
     rules, loss = so.select_bruteforce(dl, dens, 1.0, layer_of=[0, 0, 1, 1], max_rules_per_layer=1)
     assert rules == [1, 1, 0, 0] and loss == 1.5
+
+
+def test_pareto_front_hand_example():
+    # One head, four rules; per-length losses (length A, length B):
+    # r0 (1, 3), r1 (2, 2), r2 (3, 1), r3 (2, 3) -- r3 is dominated by r1.
+    dls = [np.array([[1.0, 2.0, 3.0, 2.0]]), np.array([[3.0, 2.0, 1.0, 3.0]])]
+    dens = [np.array([0.5, 0.5, 0.5, 0.5])] * 2
+    assert so.pareto_front_bruteforce(dls, dens, [1.0, None]) == [(1.0, 3.0), (2.0, 2.0), (3.0, 1.0)]
+    # a budget that only r0 and r3 meet
+    dens_b = [np.array([0.5, 0.9, 0.9, 0.5])] * 2
+    assert so.pareto_front_bruteforce(dls, dens_b, [0.6, None]) == [(1.0, 3.0)]
+    assert so.dominates((1, 2), (1, 3)) and not so.dominates((1, 3), (1, 3)) and not so.dominates((0, 4), (1, 3))
+
