@@ -45,6 +45,7 @@ namespace {
 
 constexpr int kWaves = 4;          // waves per worker (work-group)
 constexpr int kMmaKeys = 64;       // keys per wave tile in the matrix-core loop
+constexpr int kFastParts = 8;      // caches split over at most this many workers merge in one pass
 
 __device__ __forceinline__ int64_t worker_start(const DecodeArgs& a, int w) {
   return int64_t(w) * a.per_worker + (int64_t(w) * a.rem) / a.workers;
@@ -496,6 +497,44 @@ __global__ void __launch_bounds__(256) decode_combine_kernel(DecodeArgs a) {
   const int np = w1 - w0 + 1;
   const float* part0 = a.part + (int64_t(w0) + bg) * G * PS;
   auto at = [&](int p, int h) { return part0 + (int64_t(p) * G + h) * PS; };
+
+  if (np <= kFastParts) {
+    // Few partials (the common case): every thread of the first TPR loads
+    // (m, l, its float4 of acc) of all of them at once and merges in one pass.
+    if (threadIdx.x >= TPR) return;
+    const int h = threadIdx.x / V4, d4 = threadIdx.x % V4;
+    float mp[kFastParts], lp[kFastParts];
+    f32x4 xp[kFastParts];
+#pragma unroll
+    for (int p = 0; p < kFastParts; ++p) {
+      if (p < np) {
+        const float* q = at(p, h);
+        mp[p] = q[D];
+        lp[p] = q[D + 1];
+        xp[p] = *reinterpret_cast<const f32x4*>(q + 4 * d4);
+      } else {
+        mp[p] = kNegBig;
+        lp[p] = 0.0f;
+        xp[p] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
+      }
+    }
+    float mx = kNegBig;
+#pragma unroll
+    for (int p = 0; p < kFastParts; ++p) mx = fmaxf(mx, mp[p]);
+    float ls = 0.0f;
+    f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int p = 0; p < kFastParts; ++p) {
+      const float wgt = fast_exp2(mp[p] - mx);
+      ls += wgt * lp[p];
+      acc += xp[p] * wgt;
+    }
+    acc *= 1.0f / ls;
+    T* op = static_cast<T*>(a.o) + (int64_t(b) * a.hq + g * G + h) * D + 4 * d4;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) op[e] = static_cast<T>(acc[e]);
+    return;
+  }
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   for (int h = wave; h < G; h += 4) {
