@@ -386,3 +386,27 @@ def test_planted_block_mask_mistakes_are_caught():
     ]
     for m in mutants:
         assert not _golden_block_ok(m)
+
+
+def test_decode_over_the_cache_slots_in_any_order():
+    # Softmax over a set does not depend on its order: attending over the cache
+    # model's filled slots (ring order, then shuffled) gives the decode row
+    # computed from the full history.
+    n, hq, hkv, d, s = 40, 4, 2, 8, 3
+    windows = [5, 17]
+    q = _rand((1, n, hq, d), 70)
+    k = _rand((1, n, hkv, d), 71)
+    v = _rand((1, n, hkv, d), 72)
+    ref = om.decode_ref(q[:, n - 1], k, v, windows, s)
+    pos, kc, vc = om.cache_contents_ref(torch.from_numpy(k), torch.from_numpy(v), windows, s)
+    offsets = np.cumsum([0] + [w + s for w in windows])
+    rng = np.random.default_rng(5)
+    for h in range(hq):
+        g = h // (hq // hkv)
+        slots = [i for i in range(offsets[g], offsets[g + 1]) if pos[0, i] >= 0]
+        for order in (slots, list(rng.permutation(slots))):
+            ks = kc[0, order].numpy()
+            vs = vc[0, order].numpy()
+            sc = ks @ q[0, n - 1, h] / math.sqrt(d)
+            e = np.exp(sc - sc.max())
+            np.testing.assert_allclose((e / e.sum()) @ vs, ref[0, h], rtol=0, atol=1e-12)
