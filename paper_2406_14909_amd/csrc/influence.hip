@@ -17,9 +17,11 @@
 // for every calibration item in turn, then writes the block means.
 //
 // Matrix-core formulation (CDNA4 32x32x16 bf16 MFMA): S^T = K Q^T and
-// dP^T = V dO^T with the K / V tile rows as the A operand (from LDS, rows
-// padded to 272 bytes) and Q^T / dO^T kept in registers, so lane l holds
-// query row l % 32 for 16 keys and row reductions need one cross-lane step.
+// dP^T = V dO^T with the K / V tile rows as the A operand (double-buffered in
+// LDS, filled by asynchronous buffer-to-LDS loads one tile ahead, 16-byte
+// chunks XOR-swizzled per row) and Q^T / dO^T kept in registers, so lane l
+// holds query row l % 32 for 16 keys and row reductions need one cross-lane
+// step.
 // Where fp32 rounds A_ij to 1 (the row's other weights are below 2^-24 of
 // it, e.g. row 0) the influence is reported as 0.
 #include "moa_device.h"
@@ -55,12 +57,12 @@ template <int D>
 __global__ void __launch_bounds__(INW * 64, 2) influence_kernel(InfluenceArgs a) {
   constexpr int KS = D / 16;              // MFMA steps over the head dimension
   constexpr int RB = D * 2;               // bytes per K / V row
-  constexpr int RS = RB + 16;             // padded LDS row stride
   constexpr int CPR = RB / 16;            // 16-byte chunks per row
-  constexpr int LPT = IBN * CPR / (INW * 64);   // chunks per thread per tile
+  constexpr int TILE = IBN * RB;          // one K or V tile (rows unpadded)
+  constexpr int DPW = TILE / 1024 / INW;  // 1 KB direct-to-LDS loads per wave per tile
 
-  __shared__ __attribute__((aligned(16))) char sK[IBN * RS];
-  __shared__ __attribute__((aligned(16))) char sV[IBN * RS];
+  __shared__ __attribute__((aligned(1024))) char sK[2][TILE];
+  __shared__ __attribute__((aligned(1024))) char sV[2][TILE];
   __shared__ float s_part[INW][kMaxBlocks];     // per-wave block sums
 
   const int lane = threadIdx.x & 63;
@@ -86,55 +88,61 @@ __global__ void __launch_bounds__(INW * 64, 2) influence_kernel(InfluenceArgs a)
   for (int x = threadIdx.x; x < INW * kMaxBlocks; x += INW * 64) (&s_part[0][0])[x] = 0.0f;
 
   const int64_t q_stride = int64_t(a.hq) * D;     // elements between consecutive tokens
-  const int64_t kv_stride = int64_t(a.hkv) * D;
+  const uint32_t kv_row_bytes = uint32_t(a.hkv) * RB;
 
-  auto load_tiles = [&](int b, int it) {
+  // K / V rows in LDS: 16-byte chunk c of row r sits at chunk position
+  // c ^ swz(r), so the 16 rows read together by an MFMA operand load hit 16
+  // different bank groups.  Tiles arrive by asynchronous buffer-to-LDS loads:
+  // load i of this wave writes tile bytes [(wave * DPW + i) * 1024, +1024),
+  // lane L's 16 bytes landing at chunk m = (wave * DPW + i) * 64 + L (row
+  // m / CPR, position m % CPR) and carrying global chunk position ^ swz(row).
+  auto swz = [](int r) { return CPR >= 16 ? (r & 15) : ((r >> 1) & 7); };
+  uint32_t src[DPW];
+  int src_row[DPW];
+#pragma unroll
+  for (int i = 0; i < DPW; ++i) {
+    const int m = (wave * DPW + i) * 64 + lane;
+    const int r = m / CPR, pos = m % CPR;
+    src_row[i] = r;
+    src[i] = uint32_t(r) * kv_row_bytes + uint32_t(pos ^ swz(r)) * 16u;
+  }
+  // Tile `it` of item b into buffer `buf`.  The buffer resource spans exactly
+  // the tile's real key rows; rows past n re-read row n - 1 (never visible).
+  auto issue = [&](int b, int it, int buf) {
     const int j0 = it * IBN;
-    const bf16* kg = static_cast<const bf16*>(a.k) + (int64_t(b) * n * a.hkv + g) * D;
-    const bf16* vg = static_cast<const bf16*>(a.v) + (int64_t(b) * n * a.hkv + g) * D;
-    bf16x8 kr[LPT], vr[LPT];
+    const int rows = min(IBN, n - j0);
+    const int64_t first = (int64_t(b) * n + j0) * a.hkv + g;      // row j0 of head g, in rows of D
+    const i32x4 kd = make_desc(static_cast<const char*>(a.k) + first * RB, uint32_t(rows - 1) * kv_row_bytes + RB);
+    const i32x4 vd = make_desc(static_cast<const char*>(a.v) + first * RB, uint32_t(rows - 1) * kv_row_bytes + RB);
 #pragma unroll
-    for (int x = 0; x < LPT; ++x) {
-      const int c = threadIdx.x + x * INW * 64;
-      const int r = c / CPR, cc = c % CPR;
-      const int j = j0 + r;
-      if (j < n) {
-        kr[x] = *reinterpret_cast<const bf16x8*>(kg + int64_t(j) * kv_stride + cc * 8);
-        vr[x] = *reinterpret_cast<const bf16x8*>(vg + int64_t(j) * kv_stride + cc * 8);
-      } else {
-        kr[x] = bf16x8{};
-        vr[x] = bf16x8{};
-      }
+    for (int i = 0; i < DPW; ++i) {
+      const uint32_t off = src_row[i] < rows ? src[i] : src[i] - uint32_t(src_row[i] - (rows - 1)) * kv_row_bytes;
+      dma16_async(kd, off, &sK[buf][(wave * DPW + i) * 1024]);
+      dma16_async(vd, off, &sV[buf][(wave * DPW + i) * 1024]);
     }
-    __syncthreads();                              // the previous tile is no longer read
-#pragma unroll
-    for (int x = 0; x < LPT; ++x) {
-      const int c = threadIdx.x + x * INW * 64;
-      const int r = c / CPR, cc = c % CPR;
-      *reinterpret_cast<bf16x8*>(sK + r * RS + cc * 16) = kr[x];
-      *reinterpret_cast<bf16x8*>(sV + r * RS + cc * 16) = vr[x];
-    }
-    __syncthreads();
   };
 
-  // S^T and dP^T of one 64-key tile (two 32-key halves), from LDS.
-  auto products = [&](const bf16x8* qf, const bf16x8* df, f32x16* sacc, f32x16* dacc) {
+  // S^T and dP^T of one 64-key tile (two 32-key halves), from LDS buffer buf.
+  auto products = [&](int buf, const bf16x8* qf, const bf16x8* df, f32x16* sacc, f32x16* dacc) {
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
       sacc[sub] = f32x16{};
       dacc[sub] = f32x16{};
-      const char* kb = sK + (sub * 32 + lrow) * RS + 16 * half;
-      const char* vb = sV + (sub * 32 + lrow) * RS + 16 * half;
+      const int r = sub * 32 + lrow;
+      const char* kb = &sK[buf][r * RB];
+      const char* vb = &sV[buf][r * RB];
 #pragma unroll
       for (int kk = 0; kk < KS; ++kk) {
-        sacc[sub] = mma32(*reinterpret_cast<const bf16x8*>(kb + 32 * kk), qf[kk], sacc[sub]);
-        dacc[sub] = mma32(*reinterpret_cast<const bf16x8*>(vb + 32 * kk), df[kk], dacc[sub]);
+        const int off = ((2 * kk + half) ^ swz(r)) * 16;
+        sacc[sub] = mma32(*reinterpret_cast<const bf16x8*>(kb + off), qf[kk], sacc[sub]);
+        dacc[sub] = mma32(*reinterpret_cast<const bf16x8*>(vb + off), df[kk], dacc[sub]);
       }
     }
   };
   // Key of register r of half-tile `sub` held by this lane.
   auto key_of = [&](int j0, int sub, int r) { return j0 + sub * 32 + (r >> 2) * 8 + half * 4 + (r & 3); };
 
+  int cnt = 0;                                      // tiles consumed so far (buffer parity)
   for (int b = 0; b < a.batch; ++b) {
     bf16x8 qf[KS], df[KS];
     if (row_ok) {
@@ -152,64 +160,71 @@ __global__ void __launch_bounds__(INW * 64, 2) influence_kernel(InfluenceArgs a)
         df[kk] = bf16x8{};
       }
     }
+    issue(b, 0, cnt & 1);
+    // Q / dO are waited for here, once: the tile loads are invisible to the
+    // compiler's wait tracking, which would otherwise wait inside the loop.
+    __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
 
-    // Pass 1: row max, row sum and sum of e * dP (log2 domain for the max).
-    float m = kNegBig, l = 0.0f, u = 0.0f;
-    for (int it = 0; it < ntiles; ++it) {
-      load_tiles(b, it);
-      const int j0 = it * IBN;
-      if (!wave_active || j0 > iw_last) continue;
-      f32x16 sacc[2], dacc[2];
-      products(qf, df, sacc, dacc);
-      float tmax = -INFINITY;
+    float m = kNegBig, l = 0.0f, u = 0.0f, lse2 = 0.0f, drow = 0.0f;
+    for (int pass = 0; pass < 2; ++pass) {
+      for (int it = 0; it < ntiles; ++it, ++cnt) {
+        __builtin_amdgcn_s_waitcnt(0x0F70);     // this wave's loads of tile `it` have landed
+        __syncthreads();                        // ... everyone's; the other buffer is free
+        if (it + 1 < ntiles) issue(b, it + 1, (cnt + 1) & 1);
+        else if (pass == 0) issue(b, 0, (cnt + 1) & 1);
+        const int buf = cnt & 1;
+        const int j0 = it * IBN;
+        if (!wave_active || j0 > iw_last) continue;
+        f32x16 sacc[2], dacc[2];
+        products(buf, qf, df, sacc, dacc);
+        if (pass == 0) {
+          // row max, row sum and sum of e * dP (log2 domain for the max)
+          float tmax = -INFINITY;
 #pragma unroll
-      for (int sub = 0; sub < 2; ++sub)
+          for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const bool vis = row_ok && key_of(j0, sub, r) <= my_row;
-          sacc[sub][r] = vis ? sacc[sub][r] * c2 : -INFINITY;
-          tmax = fmaxf(tmax, sacc[sub][r]);
+            for (int r = 0; r < 16; ++r) {
+              const bool vis = row_ok && key_of(j0, sub, r) <= my_row;
+              sacc[sub][r] = vis ? sacc[sub][r] * c2 : -INFINITY;
+              tmax = fmaxf(tmax, sacc[sub][r]);
+            }
+          tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+          const float m_new = fmaxf(m, tmax);
+          const float alpha = fast_exp2(m - m_new);
+          l *= alpha;
+          u *= alpha;
+#pragma unroll
+          for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const float e = fast_exp2(sacc[sub][r] - m_new);
+              l += e;
+              u += e * dacc[sub][r];
+            }
+          m = m_new;
+        } else {
+          // influence, summed per (row block, key block)
+          float esum = 0.0f;
+#pragma unroll
+          for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const bool vis = row_ok && key_of(j0, sub, r) <= my_row;
+              const float p = fast_exp2(__builtin_fmaf(sacc[sub][r], c2, -lse2));
+              const float rest = 1.0f - p;
+              const float e = -p * __builtin_amdgcn_rcpf(rest) * (dacc[sub][r] - drow);
+              esum += (vis && rest > 0.0f) ? e : 0.0f;
+            }
+          esum = wave_sum(esum);
+          if (lane == 0) s_part[wave][it] += esum;
         }
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-      const float m_new = fmaxf(m, tmax);
-      const float alpha = fast_exp2(m - m_new);
-      l *= alpha;
-      u *= alpha;
-#pragma unroll
-      for (int sub = 0; sub < 2; ++sub)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float e = fast_exp2(sacc[sub][r] - m_new);
-          l += e;
-          u += e * dacc[sub][r];
-        }
-      m = m_new;
-    }
-    l += __shfl_xor(l, 32, 64);
-    u += __shfl_xor(u, 32, 64);
-    const float lse2 = m + __log2f(l);
-    const float drow = u / l;
-
-    // Pass 2: influence, summed per (row block, key block).
-    for (int it = 0; it < ntiles; ++it) {
-      load_tiles(b, it);
-      const int j0 = it * IBN;
-      if (!wave_active || j0 > iw_last) continue;
-      f32x16 sacc[2], dacc[2];
-      products(qf, df, sacc, dacc);
-      float esum = 0.0f;
-#pragma unroll
-      for (int sub = 0; sub < 2; ++sub)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const bool vis = row_ok && key_of(j0, sub, r) <= my_row;
-          const float p = fast_exp2(__builtin_fmaf(sacc[sub][r], c2, -lse2));
-          const float rest = 1.0f - p;
-          const float e = -p * __builtin_amdgcn_rcpf(rest) * (dacc[sub][r] - drow);
-          esum += (vis && rest > 0.0f) ? e : 0.0f;
-        }
-      esum = wave_sum(esum);
-      if (lane == 0) s_part[wave][it] += esum;
+      }
+      if (pass == 0) {
+        l += __shfl_xor(l, 32, 64);
+        u += __shfl_xor(u, 32, 64);
+        lse2 = m + __log2f(l);
+        drow = u / l;
+      }
     }
   }
   __syncthreads();
