@@ -12,8 +12,8 @@
 //   pass 1: S = Q K^T, dP = dO V^T; online row max m, row sum l of
 //           e = exp(S - m) and u = sum e * dP, so D_i = u / l and
 //           log-sum-exp = m + log l;
-//   pass 2: S and dP again, P = exp(S - lse), E as above, summed per
-//           (64-row block, 64-key block) into LDS,
+//   pass 2: S and dP again, A / (1 - A) = 1 / (exp(lse - S) - 1), E as
+//           above, summed per (64-row block, 64-key block) into LDS,
 // for every calibration item in turn, then writes the block means.
 //
 // Matrix-core formulation (CDNA4 32x32x16 bf16 MFMA): S^T = K Q^T and
@@ -22,8 +22,9 @@
 // chunks XOR-swizzled per row) and Q^T / dO^T kept in registers, so lane l
 // holds query row l % 32 for 16 keys and row reductions need one cross-lane
 // step.
-// Where fp32 rounds A_ij to 1 (the row's other weights are below 2^-24 of
-// it, e.g. row 0) the influence is reported as 0.
+// Where 1 - A_ij of a row's largest weight is not resolved in fp32 (the
+// row's other weights sum to less than about 2^-22 of it, e.g. row 0) the
+// influence of the whole row is reported as 0.
 #include "moa_device.h"
 
 namespace moa {
@@ -139,8 +140,8 @@ __global__ void __launch_bounds__(INW * 64, 2) influence_kernel(InfluenceArgs a)
       }
     }
   };
-  // Key of register r of half-tile `sub` held by this lane.
-  auto key_of = [&](int j0, int sub, int r) { return j0 + sub * 32 + (r >> 2) * 8 + half * 4 + (r & 3); };
+  // Register r of half-tile `sub` holds, for this lane's query row, the key
+  // j0 + sub * 32 + (r / 4) * 8 + half * 4 + r % 4 (32x32 MFMA output layout).
 
   int cnt = 0;                                      // tiles consumed so far (buffer parity)
   for (int b = 0; b < a.batch; ++b) {
@@ -165,7 +166,10 @@ __global__ void __launch_bounds__(INW * 64, 2) influence_kernel(InfluenceArgs a)
     // compiler's wait tracking, which would otherwise wait inside the loop.
     __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
 
-    float m = kNegBig, l = 0.0f, u = 0.0f, lse2 = 0.0f, drow = 0.0f;
+    // Running state per query row (both wave halves hold the same row):
+    // mr = largest raw score so far, l = sum of exp2(c2 * s - c2 * mr),
+    // u = sum of those weights times dP.
+    float mr = kNegBig, l = 0.0f, u = 0.0f, lse2 = 0.0f, drow = 0.0f;
     for (int pass = 0; pass < 2; ++pass) {
       for (int it = 0; it < ntiles; ++it, ++cnt) {
         __builtin_amdgcn_s_waitcnt(0x0F70);     // this wave's loads of tile `it` have landed
@@ -177,53 +181,67 @@ __global__ void __launch_bounds__(INW * 64, 2) influence_kernel(InfluenceArgs a)
         if (!wave_active || j0 > iw_last) continue;
         f32x16 sacc[2], dacc[2];
         products(buf, qf, df, sacc, dacc);
+        // Only a tile reaching past the wave's first row holds keys after
+        // some of its rows; there a hidden score becomes -inf, which both
+        // passes below turn into a zero weight and a zero influence.
+        if (j0 + IBN - 1 > iw0) {
+          const int lim = my_row - j0 - half * 4;
+#pragma unroll
+          for (int sub = 0; sub < 2; ++sub)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              if (sub * 32 + (r >> 2) * 8 + (r & 3) > lim) sacc[sub][r] = -INFINITY;
+        }
         if (pass == 0) {
-          // row max, row sum and sum of e * dP (log2 domain for the max)
           float tmax = -INFINITY;
 #pragma unroll
           for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const bool vis = row_ok && key_of(j0, sub, r) <= my_row;
-              sacc[sub][r] = vis ? sacc[sub][r] * c2 : -INFINITY;
-              tmax = fmaxf(tmax, sacc[sub][r]);
-            }
+            for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, sacc[sub][r]);
           tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-          const float m_new = fmaxf(m, tmax);
-          const float alpha = fast_exp2(m - m_new);
+          const float mr_new = fmaxf(mr, tmax);
+          const float m_new = mr_new * c2;          // scale > 0: the scaled maximum
+          const float alpha = fast_exp2(mr * c2 - m_new);
           l *= alpha;
           u *= alpha;
 #pragma unroll
           for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-              const float e = fast_exp2(sacc[sub][r] - m_new);
+              const float e = fast_exp2(__builtin_fmaf(sacc[sub][r], c2, -m_new));
               l += e;
-              u += e * dacc[sub][r];
+              u = __builtin_fmaf(e, dacc[sub][r], u);
             }
-          m = m_new;
+          mr = mr_new;
         } else {
-          // influence, summed per (row block, key block)
-          float esum = 0.0f;
+          // A / (1 - A) = 1 / (2^(lse2 - c2 s) - 1), so the tile's influence
+          // sum is  sum -ratio * (dP - D) = D * sum ratio - sum ratio * dP.
+          float acc_dp = 0.0f, acc_r = 0.0f;
 #pragma unroll
           for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
-              const bool vis = row_ok && key_of(j0, sub, r) <= my_row;
-              const float p = fast_exp2(__builtin_fmaf(sacc[sub][r], c2, -lse2));
-              const float rest = 1.0f - p;
-              const float e = -p * __builtin_amdgcn_rcpf(rest) * (dacc[sub][r] - drow);
-              esum += (vis && rest > 0.0f) ? e : 0.0f;
+              const float inv_p = fast_exp2(__builtin_fmaf(sacc[sub][r], -c2, lse2));
+              const float ratio = __builtin_amdgcn_rcpf(inv_p - 1.0f);
+              acc_dp = __builtin_fmaf(ratio, dacc[sub][r], acc_dp);
+              acc_r += ratio;
             }
-          esum = wave_sum(esum);
+          const float esum = wave_sum(__builtin_fmaf(drow, acc_r, -acc_dp));
           if (lane == 0) s_part[wave][it] += esum;
         }
       }
       if (pass == 0) {
         l += __shfl_xor(l, 32, 64);
         u += __shfl_xor(u, 32, 64);
-        lse2 = m + __log2f(l);
+        lse2 = mr * c2 + __log2f(l);
         drow = u / l;
+        // 1 / A of the row's largest weight, computed exactly as the second
+        // pass will.  Where it lies within two fp32 ulps of 1, 1 - A is not
+        // resolved: the whole row is reported as 0 (lse2 = +inf makes every
+        // ratio 0), as is a row past n.  Elsewhere every key's 1 / A exceeds
+        // 1, so no ratio divides by zero.
+        const float inv_p_max = fast_exp2(__builtin_fmaf(mr, -c2, lse2));
+        if (!row_ok || !(inv_p_max - 1.0f >= 0x1p-22f)) lse2 = INFINITY;
       }
     }
   }
