@@ -303,9 +303,10 @@ def main() -> int:
 
 def measure_influence(args):
     """Times moa_influence (dense causal attention of the workload's layer shape,
-    bf16) over a batch of calibration items.  Algorithmic work: two passes of
-    two products (Q K^T and dO V^T), 8 * head_dim flops per causal (query,
-    key) pair per item and query head."""
+    bf16) over a batch of calibration items, after at least 3 untimed calls
+    (the first calls run before the clocks have settled).  Algorithmic work:
+    two passes of two products (Q K^T and dO V^T), 8 * head_dim flops per
+    causal (query, key) pair per item and query head."""
     import torch
 
     sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
@@ -319,7 +320,7 @@ def measure_influence(args):
     v = workloads.randn((items, n, hkv, d), 13, torch.bfloat16, "cuda")
     do = workloads.randn((items, n, hq, d), 14, torch.bfloat16, "cuda")
     ebar = M.moa_influence(q, k, v, do)
-    for _ in range(max(1, args.warmup)):
+    for _ in range(max(3, args.warmup)):
         M.moa_influence(q, k, v, do, ebar)
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
@@ -361,7 +362,7 @@ def measure_rule_loss(args):
     ebar = torch.randn((heads, nb, nb), generator=gen, device="cuda").tril_()
     a, b = search.candidate_rules()
     flags = M.MOA_BLOCK_BAND | M.MOA_SPAN_INCLUDES_SINKS
-    for _ in range(max(1, args.warmup)):
+    for _ in range(max(3, args.warmup)):
         M.moa_rule_loss(ebar, n, 64, a, b, flags)
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()

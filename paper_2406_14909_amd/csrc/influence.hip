@@ -25,6 +25,8 @@
 // Where 1 - A_ij of a row's largest weight is not resolved in fp32 (the
 // row's other weights sum to less than about 2^-22 of it, e.g. row 0) the
 // influence of the whole row is reported as 0.
+#include <type_traits>
+
 #include "moa_device.h"
 
 namespace moa {
@@ -52,6 +54,14 @@ __device__ __forceinline__ float wave_sum(float x) {
   x += __shfl_xor(x, 16, 64);
   x += __shfl_xor(x, 32, 64);
   return x;
+}
+
+// Nothing is scheduled across this point: it keeps the written interleave
+// of matrix products and vector work.
+__device__ __forceinline__ void sched_fence() {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_sched_barrier(0);
+#endif
 }
 
 template <int D>
@@ -98,50 +108,89 @@ __global__ void __launch_bounds__(INW * 64, 2) influence_kernel(InfluenceArgs a)
   // lane L's 16 bytes landing at chunk m = (wave * DPW + i) * 64 + L (row
   // m / CPR, position m % CPR) and carrying global chunk position ^ swz(row).
   auto swz = [](int r) { return CPR >= 16 ? (r & 15) : ((r >> 1) & 7); };
-  uint32_t src[DPW];
+  uint32_t chunk_off[DPW];
   int src_row[DPW];
 #pragma unroll
   for (int i = 0; i < DPW; ++i) {
     const int m = (wave * DPW + i) * 64 + lane;
     const int r = m / CPR, pos = m % CPR;
     src_row[i] = r;
-    src[i] = uint32_t(r) * kv_row_bytes + uint32_t(pos ^ swz(r)) * 16u;
+    chunk_off[i] = uint32_t(pos ^ swz(r)) * 16u;
   }
-  // Tile `it` of item b into buffer `buf`.  The buffer resource spans exactly
-  // the tile's real key rows; rows past n re-read row n - 1 (never visible).
+  // Tile `it` of item b into buffer `buf`.  The buffer resource spans the
+  // item's n key rows of head g; rows past n re-read row n - 1 (never
+  // visible).
+  const uint32_t span = uint32_t(n - 1) * kv_row_bytes + RB;
   auto issue = [&](int b, int it, int buf) {
-    const int j0 = it * IBN;
-    const int rows = min(IBN, n - j0);
-    const int64_t first = (int64_t(b) * n + j0) * a.hkv + g;      // row j0 of head g, in rows of D
-    const i32x4 kd = make_desc(static_cast<const char*>(a.k) + first * RB, uint32_t(rows - 1) * kv_row_bytes + RB);
-    const i32x4 vd = make_desc(static_cast<const char*>(a.v) + first * RB, uint32_t(rows - 1) * kv_row_bytes + RB);
+    const int64_t first = int64_t(b) * n * a.hkv + g;             // row 0 of head g, in rows of D
+    const i32x4 kd = make_desc(static_cast<const char*>(a.k) + first * RB, span);
+    const i32x4 vd = make_desc(static_cast<const char*>(a.v) + first * RB, span);
 #pragma unroll
     for (int i = 0; i < DPW; ++i) {
-      const uint32_t off = src_row[i] < rows ? src[i] : src[i] - uint32_t(src_row[i] - (rows - 1)) * kv_row_bytes;
+      const uint32_t off = uint32_t(min(it * IBN + src_row[i], n - 1)) * kv_row_bytes + chunk_off[i];
       dma16_async(kd, off, &sK[buf][(wave * DPW + i) * 1024]);
       dma16_async(vd, off, &sV[buf][(wave * DPW + i) * 1024]);
     }
   };
 
-  // S^T and dP^T of one 64-key tile (two 32-key halves), from LDS buffer buf.
-  auto products = [&](int buf, const bf16x8* qf, const bf16x8* df, f32x16* sacc, f32x16* dacc) {
-#pragma unroll
-    for (int sub = 0; sub < 2; ++sub) {
-      sacc[sub] = f32x16{};
-      dacc[sub] = f32x16{};
-      const int r = sub * 32 + lrow;
-      const char* kb = &sK[buf][r * RB];
-      const char* vb = &sV[buf][r * RB];
-#pragma unroll
-      for (int kk = 0; kk < KS; ++kk) {
-        const int off = ((2 * kk + half) ^ swz(r)) * 16;
-        sacc[sub] = mma32(*reinterpret_cast<const bf16x8*>(kb + off), qf[kk], sacc[sub]);
-        dacc[sub] = mma32(*reinterpret_cast<const bf16x8*>(vb + off), df[kk], dacc[sub]);
-      }
-    }
+  struct Acc {                                    // S^T and dP^T of 32 keys
+    f32x16 s, d;
   };
-  // Register r of half-tile `sub` holds, for this lane's query row, the key
-  // j0 + sub * 32 + (r / 4) * 8 + half * 4 + r % 4 (32x32 MFMA output layout).
+  // Register r of a 32-key half holds, for this lane's query row, key
+  // (r / 4) * 8 + half * 4 + r % 4 of the half (32x32 MFMA output layout).
+  // On the diagonal half (keys iw0 .. iw0 + 31) a key after the row gets
+  // score -inf, which both passes turn into zero weight and zero influence.
+  auto mask_diagonal = [&](Acc& acc) {
+    const int lim = lrow - half * 4;
+#pragma unroll
+    for (int r = 0; r < 16; ++r)
+      if ((r >> 2) * 8 + (r & 3) > lim) acc.s[r] = -INFINITY;
+  };
+
+  // Running state per query row (both wave halves hold the same row):
+  // mr = largest raw score so far, l = sum of exp2(c2 * s - c2 * mr),
+  // u = sum of those weights times dP; in pass 2, sums of ratio * dP and of
+  // ratio over the current 64-key tile.
+  float mr, l, u, lse2, drow, acc_dp, acc_r;
+  // Pass 1, one 32-key half: new running maximum (returns the scaled one),
+  // then each element's weight.
+  auto rescale = [&](const Acc& acc) {
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, acc.s[r]);
+    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    const float mr_new = fmaxf(mr, tmax);
+    const float m_new = mr_new * c2;              // scale > 0: the scaled maximum
+    const float alpha = fast_exp2(mr * c2 - m_new);
+    l *= alpha;
+    u *= alpha;
+    mr = mr_new;
+    return m_new;
+  };
+  auto weigh = [&](float sv, float dv, float m_new) {
+    const float e = fast_exp2(__builtin_fmaf(sv, c2, -m_new));
+    l += e;
+    u = __builtin_fmaf(e, dv, u);
+  };
+  // Pass 2, one element: A / (1 - A) = 1 / (2^(lse2 - c2 s) - 1), and the
+  // tile's influence sum is  sum -ratio * (dP - D) = D * sum ratio - sum ratio * dP.
+  auto influence = [&](float sv, float dv) {
+    const float inv_p = fast_exp2(__builtin_fmaf(sv, -c2, lse2));
+    const float ratio = __builtin_amdgcn_rcpf(inv_p - 1.0f);
+    acc_dp = __builtin_fmaf(ratio, dv, acc_dp);
+    acc_r += ratio;
+  };
+  auto flush_tile = [&](int t) {
+    const float esum = wave_sum(__builtin_fmaf(drow, acc_r, -acc_dp));
+    if (lane == 0) s_part[wave][t] += esum;
+    acc_dp = 0.0f;
+    acc_r = 0.0f;
+  };
+
+  // Keys 0 .. iw0 - 1 precede every row of the wave: iw0 / 32 halves need no
+  // mask.  The half after them is the diagonal one; later keys are hidden.
+  const int n_plain = wave_active ? iw0 / 32 : 0;
+  const int n_pairs = n_plain / 2;
 
   int cnt = 0;                                      // tiles consumed so far (buffer parity)
   for (int b = 0; b < a.batch; ++b) {
@@ -161,90 +210,126 @@ __global__ void __launch_bounds__(INW * 64, 2) influence_kernel(InfluenceArgs a)
         df[kk] = bf16x8{};
       }
     }
-    issue(b, 0, cnt & 1);
+    if (b == 0) issue(b, 0, cnt & 1);       // later items' first tiles come with the previous pass
     // Q / dO are waited for here, once: the tile loads are invisible to the
     // compiler's wait tracking, which would otherwise wait inside the loop.
     __builtin_amdgcn_s_waitcnt(0x0F70);   // vmcnt(0)
 
-    // Running state per query row (both wave halves hold the same row):
-    // mr = largest raw score so far, l = sum of exp2(c2 * s - c2 * mr),
-    // u = sum of those weights times dP.
-    float mr = kNegBig, l = 0.0f, u = 0.0f, lse2 = 0.0f, drow = 0.0f;
-    for (int pass = 0; pass < 2; ++pass) {
-      for (int it = 0; it < ntiles; ++it, ++cnt) {
-        __builtin_amdgcn_s_waitcnt(0x0F70);     // this wave's loads of tile `it` have landed
-        __syncthreads();                        // ... everyone's; the other buffer is free
-        if (it + 1 < ntiles) issue(b, it + 1, (cnt + 1) & 1);
-        else if (pass == 0) issue(b, 0, (cnt + 1) & 1);
-        const int buf = cnt & 1;
-        const int j0 = it * IBN;
-        if (!wave_active || j0 > iw_last) continue;
-        f32x16 sacc[2], dacc[2];
-        products(buf, qf, df, sacc, dacc);
-        // Only a tile reaching past the wave's first row holds keys after
-        // some of its rows; there a hidden score becomes -inf, which both
-        // passes below turn into a zero weight and a zero influence.
-        if (j0 + IBN - 1 > iw0) {
-          const int lim = my_row - j0 - half * 4;
+    mr = kNegBig;
+    l = u = lse2 = drow = acc_dp = acc_r = 0.0f;
+
+    // One pipelined step: the products of half `sub` of LDS buffer `buf`
+    // into `out` (kProd), written interleaved with the vector work of the
+    // previous half `in` (kWork) in KS groups: each group reads the operands
+    // of two groups later from LDS, issues its two MFMAs and then 16 / KS elements of
+    // vector work, which run while the matrix core is busy.  The scheduling
+    // barrier after each group keeps that order.
+    auto step = [&](auto second_c, auto prod_c, auto work_c, int buf, int sub, Acc& out, const Acc& in) {
+      constexpr bool kSecond = decltype(second_c)::value;
+      constexpr bool kProd = decltype(prod_c)::value;
+      constexpr bool kWork = decltype(work_c)::value;
+      constexpr int EPG = 16 / KS;                  // elements of work per group
+      const int r = sub * 32 + lrow;
+      const char* kb = &sK[buf][r * RB];
+      const char* vb = &sV[buf][r * RB];
+      auto frag = [&](const char* base, int kk) {
+        return *reinterpret_cast<const bf16x8*>(base + ((2 * kk + half) ^ swz(r)) * 16);
+      };
+      bf16x8 kf[3], vf[3];                          // operands read two groups ahead
+      float m_new = 0.0f;
+      if constexpr (kProd) {
+        out.s = f32x16{};
+        out.d = f32x16{};
 #pragma unroll
-          for (int sub = 0; sub < 2; ++sub)
-#pragma unroll
-            for (int r = 0; r < 16; ++r)
-              if (sub * 32 + (r >> 2) * 8 + (r & 3) > lim) sacc[sub][r] = -INFINITY;
+        for (int kk = 0; kk < 2; ++kk) {
+          kf[kk] = frag(kb, kk);
+          vf[kk] = frag(vb, kk);
         }
-        if (pass == 0) {
-          float tmax = -INFINITY;
+      }
+      if constexpr (kWork && !kSecond) m_new = rescale(in);
 #pragma unroll
-          for (int sub = 0; sub < 2; ++sub)
+      for (int kk = 0; kk < KS; ++kk) {
+        if constexpr (kProd) {
+          if (kk + 2 < KS) {
+            kf[(kk + 2) % 3] = frag(kb, kk + 2);
+            vf[(kk + 2) % 3] = frag(vb, kk + 2);
+          }
+          out.s = mma32(kf[kk % 3], qf[kk], out.s);
+          out.d = mma32(vf[kk % 3], df[kk], out.d);
+        }
+        if constexpr (kWork) {
 #pragma unroll
-            for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, sacc[sub][r]);
-          tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
-          const float mr_new = fmaxf(mr, tmax);
-          const float m_new = mr_new * c2;          // scale > 0: the scaled maximum
-          const float alpha = fast_exp2(mr * c2 - m_new);
-          l *= alpha;
-          u *= alpha;
-#pragma unroll
-          for (int sub = 0; sub < 2; ++sub)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const float e = fast_exp2(__builtin_fmaf(sacc[sub][r], c2, -m_new));
-              l += e;
-              u = __builtin_fmaf(e, dacc[sub][r], u);
-            }
-          mr = mr_new;
+          for (int e = 0; e < EPG; ++e) {
+            const int rr = kk * EPG + e;
+            if constexpr (kSecond) influence(in.s[rr], in.d[rr]);
+            else weigh(in.s[rr], in.d[rr], m_new);
+          }
+        }
+        sched_fence();
+      }
+    };
+
+    // One pass over the wave's key halves, software-pipelined: the products
+    // of half k + 1 are computed in the same step as the vector work of half
+    // k.  Every wave meets the work-group barrier once per tile of the
+    // work-group (all ntiles of them), which is when the tile's loads are
+    // complete and the next tile starts loading into the other buffer.
+    auto run_pass = [&](auto second_c) {
+      constexpr bool kSecond = decltype(second_c)::value;
+      const std::true_type yes;
+      const std::false_type no;
+      auto buf = [&](int t) { return (cnt + t) & 1; };
+      // The load issued after a pass's last tile is tile 0 of the next pass
+      // or item (past the last item: this item's tile 0 again, unused), so
+      // the loop body holds no branch.
+      auto tile_ready = [&](int t) {
+        __builtin_amdgcn_s_waitcnt(0x0F70);   // this wave's loads of tile t have landed
+        __syncthreads();                      // ... everyone's; tile t - 1's buffer is free
+        const bool last = t + 1 >= ntiles;
+        const int next_b = (last && kSecond) ? min(b + 1, a.batch - 1) : b;
+        issue(next_b, last ? 0 : t + 1, buf(t + 1));
+      };
+      Acc acc0, acc1;
+      tile_ready(0);
+      if (wave_active) {
+        step(second_c, yes, no, buf(0), 0, acc0, acc1);
+        for (int t = 0; t < n_pairs; ++t) {
+          step(second_c, yes, yes, buf(t), 1, acc1, acc0);
+          tile_ready(t + 1);
+          step(second_c, yes, yes, buf(t + 1), 0, acc0, acc1);
+          if constexpr (kSecond) flush_tile(t);
+        }
+        // Tile n_pairs: one more plain half when n_plain is odd, then the
+        // diagonal half.
+        if (n_plain & 1) {
+          step(second_c, yes, yes, buf(n_pairs), 1, acc1, acc0);
+          mask_diagonal(acc1);
+          step(second_c, no, yes, 0, 0, acc0, acc1);
         } else {
-          // A / (1 - A) = 1 / (2^(lse2 - c2 s) - 1), so the tile's influence
-          // sum is  sum -ratio * (dP - D) = D * sum ratio - sum ratio * dP.
-          float acc_dp = 0.0f, acc_r = 0.0f;
-#pragma unroll
-          for (int sub = 0; sub < 2; ++sub)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) {
-              const float inv_p = fast_exp2(__builtin_fmaf(sacc[sub][r], -c2, lse2));
-              const float ratio = __builtin_amdgcn_rcpf(inv_p - 1.0f);
-              acc_dp = __builtin_fmaf(ratio, dacc[sub][r], acc_dp);
-              acc_r += ratio;
-            }
-          const float esum = wave_sum(__builtin_fmaf(drow, acc_r, -acc_dp));
-          if (lane == 0) s_part[wave][it] += esum;
+          mask_diagonal(acc0);
+          step(second_c, no, yes, 0, 0, acc1, acc0);
         }
+        if constexpr (kSecond) flush_tile(n_pairs);
       }
-      if (pass == 0) {
-        l += __shfl_xor(l, 32, 64);
-        u += __shfl_xor(u, 32, 64);
-        lse2 = mr * c2 + __log2f(l);
-        drow = u / l;
-        // 1 / A of the row's largest weight, computed exactly as the second
-        // pass will.  Where it lies within two fp32 ulps of 1, 1 - A is not
-        // resolved: the whole row is reported as 0 (lse2 = +inf makes every
-        // ratio 0), as is a row past n.  Elsewhere every key's 1 / A exceeds
-        // 1, so no ratio divides by zero.
-        const float inv_p_max = fast_exp2(__builtin_fmaf(mr, -c2, lse2));
-        if (!row_ok || !(inv_p_max - 1.0f >= 0x1p-22f)) lse2 = INFINITY;
-      }
-    }
+      for (int t = (wave_active ? n_pairs : 0) + 1; t < ntiles; ++t) tile_ready(t);
+      cnt += ntiles;
+    };
+
+    run_pass(std::false_type{});
+    l += __shfl_xor(l, 32, 64);
+    u += __shfl_xor(u, 32, 64);
+    lse2 = mr * c2 + __log2f(l);
+    drow = u / l;
+    // 1 / A of the row's largest weight, computed exactly as the second pass
+    // will.  Where it lies within two fp32 ulps of 1, 1 - A is not resolved:
+    // the whole row is reported as 0 (lse2 = +inf makes every ratio 0), as is
+    // a row past n.  Elsewhere every key's 1 / A exceeds 1, so no ratio
+    // divides by zero.
+    const float inv_p_max = fast_exp2(__builtin_fmaf(mr, -c2, lse2));
+    if (!row_ok || !(inv_p_max - 1.0f >= 0x1p-22f)) lse2 = INFINITY;
+    run_pass(std::true_type{});
   }
+  __builtin_amdgcn_s_waitcnt(0x0F70);       // the unused last load lands before LDS is released
   __syncthreads();
 
   // Block means of the (up to) two 64-row blocks of this tile; blocks above

@@ -111,8 +111,8 @@ __device__ __forceinline__ i32x4 make_desc(const void* base, uint32_t bytes) {
 // LDS write nor waits for it before unrelated LDS reads; the caller orders it
 // with s_waitcnt vmcnt and a work-group barrier before the data is read.
 // It sets M0 itself; a kernel using it must have no other M0 user whose value
-// lives across the call (the prefill kernel has none: its only M0 writes are
-// these).
+// lives across the call (the prefill and influence kernels have none: their
+// only M0 writes are these).
 __device__ __forceinline__ void dma16_async(i32x4 desc, uint32_t voffset, void* lds_base) {
 #if defined(__HIP_DEVICE_COMPILE__)
   typedef __attribute__((address_space(3))) char lds_char;
