@@ -184,8 +184,8 @@ __global__ void __launch_bounds__(kWaves * 64) decode_valu_kernel(DecodeArgs a) 
       for (int u = 0; u < U; ++u) {
         const int r = r0 + u * STEP;
         if (r < hi) {
-          kv[u] = load16(kbase + int64_t(r) * D);
-          vv[u] = load16(vbase + int64_t(r) * D);
+          kv[u] = load16_stream(kbase + int64_t(r) * D);
+          vv[u] = load16_stream(vbase + int64_t(r) * D);
         } else {
           kv[u] = zero16<T>();
           vv[u] = zero16<T>();
@@ -373,7 +373,7 @@ __global__ void __launch_bounds__(kWaves * 64, 2) decode_mma_kernel(DecodeArgs a
         if (key < hi) {
           const bf16* kr = kb + int64_t(key) * D + 8 * q4;
 #pragma unroll
-          for (int kk = 0; kk < KS; ++kk) kop[st][kk] = *reinterpret_cast<const bf16x8*>(kr + 32 * kk);
+          for (int kk = 0; kk < KS; ++kk) kop[st][kk] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(kr + 32 * kk));
         } else {
 #pragma unroll
           for (int kk = 0; kk < KS; ++kk) kop[st][kk] = bf16x8{};
@@ -385,7 +385,8 @@ __global__ void __launch_bounds__(kWaves * 64, 2) decode_mma_kernel(DecodeArgs a
       for (int u = 0; u < VLD; ++u) {
         const int m = u * 64 + lane;
         const int key = t0 + m / CPR;
-        vr[u] = key < hi ? *reinterpret_cast<const bf16x8*>(vb + int64_t(key) * D + (m % CPR) * 8) : bf16x8{};
+        vr[u] = key < hi ? __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(vb + int64_t(key) * D + (m % CPR) * 8))
+                         : bf16x8{};
       }
 
       f32x4 s[4];
