@@ -21,7 +21,9 @@
 // LDS, filled by asynchronous buffer-to-LDS loads one tile ahead, 16-byte
 // chunks XOR-swizzled per row) and Q^T / dO^T kept in registers, so lane l
 // holds query row l % 32 for 16 keys and row reductions need one cross-lane
-// step.
+// step.  Each pass is software-pipelined over 32-key halves: the products of
+// the next half are written interleaved with the vector work on the current
+// one, so the matrix cores and the vector unit of a wave overlap.
 // Where 1 - A_ij of a row's largest weight is not resolved in fp32 (the
 // row's other weights sum to less than about 2^-22 of it, e.g. row 0) the
 // influence of the whole row is reported as 0.
@@ -90,7 +92,6 @@ __global__ void __launch_bounds__(INW * 64, 2) influence_kernel(InfluenceArgs a)
   const int i1 = min(n, i0 + IBM);
   const int iw0 = i0 + wave * 32;
   const bool wave_active = iw0 < i1;
-  const int iw_last = min(i1, iw0 + 32) - 1;
   const int my_row = iw0 + lrow;
   const bool row_ok = wave_active && my_row < n;
   const int ntiles = (i1 - 1) / IBN + 1;
