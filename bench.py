@@ -418,16 +418,22 @@ def measure_peaks():
     src = torch.ones((4 << 30) // 2, device="cuda", dtype=torch.bfloat16)
     dst = torch.empty_like(src)
     copy_ms = best_ms(lambda: dst.copy_(src))
-    probe = os.path.join(ROOT, "paper_2406_14909_amd", "_build", "stream_read")
-    stream_best = None
-    if os.path.exists(probe):
+    def calibration(name):
+        """Runs a calibration program of the package (built by build()); its "best" figure."""
+        probe = os.path.join(ROOT, "paper_2406_14909_amd", "_build", name)
+        if not os.path.exists(probe):
+            return None
         import subprocess
         out = subprocess.run([probe], capture_output=True, text=True, timeout=120).stdout
         log(out.strip())
         best = [line.split()[1] for line in out.splitlines() if line.startswith("best ")]
-        stream_best = float(best[0]) if best else None
+        return float(best[0]) if best else None
+
+    stream_best = calibration("stream_read")
+    mfma_best = calibration("mfma_loop")
     return {
         "hip_stream_read_gbs": stream_best,
+        "hip_mfma_loop_bf16_tflops": mfma_best,
         "gemm_bf16_16384_tflops": round(2.0 * n ** 3 / (gemm_ms / 1e3) / 1e12, 1),
         "stream_read_gbs": round((8 << 30) / (read_ms / 1e3) / 1e9, 1),
         "copy_read_plus_write_gbs": round(2 * (4 << 30) / (copy_ms / 1e3) / 1e9, 1),

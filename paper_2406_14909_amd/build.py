@@ -17,9 +17,9 @@ CSRC = os.path.join(PKG_DIR, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(PKG_DIR, "_build")
 LIB_PATH = os.path.join(PKG_DIR, "libmoa.so")
-# Measurement helper (not part of the library): the streaming-read ceiling.
-PROBE_SRC = os.path.join(PKG_DIR, "calibration", "stream_read.hip")
-PROBE_PATH = os.path.join(BUILD_DIR, "stream_read")
+# Measurement helpers (not part of the library): the streaming-read and
+# matrix-core ceilings of the GPU.
+PROBES = ["stream_read", "mfma_loop"]
 
 HIP_SOURCES = ["kv_append.hip", "decode.hip", "prefill.hip", "influence.hip", "rule_loss.hip"]
 HOST_SOURCES = ["moa_api.cpp"]
@@ -72,8 +72,9 @@ def build(verbose: bool = False) -> str:
             print(" ".join(c))
     _run_all(cmds)
     tmp = LIB_PATH + ".tmp"
-    _run_all([[HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs],
-              [HIPCC, *HIP_FLAGS, PROBE_SRC, "-o", PROBE_PATH]])
+    _run_all([[HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]] +
+             [[HIPCC, *HIP_FLAGS, os.path.join(PKG_DIR, "calibration", p + ".hip"), "-o", os.path.join(BUILD_DIR, p)]
+              for p in PROBES])
     shutil.move(tmp, LIB_PATH)
     return LIB_PATH
 
