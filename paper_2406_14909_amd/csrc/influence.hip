@@ -51,13 +51,6 @@ __device__ __forceinline__ f32x16 mma32(const bf16x8& a, const bf16x8& b, const 
 #endif
 }
 
-__device__ __forceinline__ float wave_sum(float x) {
-  x = group_sum<16>(x);
-  x += __shfl_xor(x, 16, 64);
-  x += __shfl_xor(x, 32, 64);
-  return x;
-}
-
 // Nothing is scheduled across this point: it keeps the written interleave
 // of matrix products and vector work.
 __device__ __forceinline__ void sched_fence() {
@@ -159,7 +152,7 @@ __global__ void __launch_bounds__(INW * 64, 2) influence_kernel(InfluenceArgs a)
     float tmax = -INFINITY;
 #pragma unroll
     for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, acc.s[r]);
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+    tmax = max_halves(tmax);
     const float mr_new = fmaxf(mr, tmax);
     const float m_new = mr_new * c2;              // scale > 0: the scaled maximum
     const float alpha = fast_exp2(mr * c2 - m_new);
@@ -182,8 +175,8 @@ __global__ void __launch_bounds__(INW * 64, 2) influence_kernel(InfluenceArgs a)
     acc_r += ratio;
   };
   auto flush_tile = [&](int t) {
-    const float esum = wave_sum(__builtin_fmaf(drow, acc_r, -acc_dp));
-    if (lane == 0) s_part[wave][t] += esum;
+    const float esum = wave_sum_lane63(__builtin_fmaf(drow, acc_r, -acc_dp));
+    if (lane == 63) s_part[wave][t] += esum;
     acc_dp = 0.0f;
     acc_r = 0.0f;
   };
@@ -317,8 +310,8 @@ __global__ void __launch_bounds__(INW * 64, 2) influence_kernel(InfluenceArgs a)
     };
 
     run_pass(std::false_type{});
-    l += __shfl_xor(l, 32, 64);
-    u += __shfl_xor(u, 32, 64);
+    l = sum_halves(l);
+    u = sum_halves(u);
     lse2 = mr * c2 + __log2f(l);
     drow = u / l;
     // 1 / A of the row's largest weight, computed exactly as the second pass

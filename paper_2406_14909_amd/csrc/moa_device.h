@@ -162,4 +162,48 @@ __device__ __forceinline__ float group_sum(float x) {
   return x;
 }
 
+// The two halves of a wave exchanged: lane l gets (x of lane l mod 32,
+// x of lane 32 + l mod 32), the lane's own value and that of lane l ^ 32 in
+// one fixed order, so a symmetric combination of the pair is bit-identical in
+// both halves.  One v_permlane32_swap (a vector-ALU exchange of the halves)
+// replaces an LDS permute, whose wait would also wait for every LDS read
+// issued before it.  Checked on gfx950: with both operands holding x the
+// instruction leaves [x_0..31, x_0..31] in the first and [x_32..63,
+// x_32..63] in the second.  Written as assembly with its own wait states
+// around it; the compiler builtin for it returned its second result wrong.
+struct HalfPair {
+  float lo, hi;
+};
+__device__ __forceinline__ HalfPair wave_halves(float x) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  unsigned a = __builtin_bit_cast(unsigned, x), b = a;
+  asm("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+  return {__builtin_bit_cast(float, a), __builtin_bit_cast(float, b)};
+#else
+  return {x, x};
+#endif
+}
+__device__ __forceinline__ float max_halves(float x) {
+  const HalfPair p = wave_halves(x);
+  return fmaxf(p.lo, p.hi);
+}
+__device__ __forceinline__ float sum_halves(float x) {
+  const HalfPair p = wave_halves(x);
+  return p.lo + p.hi;
+}
+
+// Sum over the 64 lanes, complete in lane 63 only: row sums within each
+// row of 16 lanes, then row_bcast:15 adds row 0 into row 1 and row 2 into
+// row 3, and row_bcast:31 adds lane 31 (rows 0 and 1) into rows 2 and 3.
+template <int ctrl, int row_mask>
+__device__ __forceinline__ float dpp_rows(float x) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, x), ctrl, row_mask, 0xF, true));
+}
+__device__ __forceinline__ float wave_sum_lane63(float x) {
+  x = group_sum<16>(x);
+  x += dpp_rows<0x142, 0xA>(x);
+  x += dpp_rows<0x143, 0xC>(x);
+  return x;
+}
+
 }  // namespace moa
