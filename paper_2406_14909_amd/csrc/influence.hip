@@ -51,14 +51,6 @@ __device__ __forceinline__ f32x16 mma32(const bf16x8& a, const bf16x8& b, const 
 #endif
 }
 
-// Nothing is scheduled across this point: it keeps the written interleave
-// of matrix products and vector work.
-__device__ __forceinline__ void sched_fence() {
-#if defined(__HIP_DEVICE_COMPILE__)
-  __builtin_amdgcn_sched_barrier(0);
-#endif
-}
-
 template <int D>
 __global__ void __launch_bounds__(INW * 64, 2) influence_kernel(InfluenceArgs a) {
   constexpr int KS = D / 16;              // MFMA steps over the head dimension

@@ -162,6 +162,14 @@ __device__ __forceinline__ float group_sum(float x) {
   return x;
 }
 
+// Nothing is scheduled across this point: it keeps a written interleave of
+// matrix products and vector work in the order written.
+__device__ __forceinline__ void sched_fence() {
+#if defined(__HIP_DEVICE_COMPILE__)
+  __builtin_amdgcn_sched_barrier(0);
+#endif
+}
+
 // The two halves of a wave exchanged: lane l gets (x of lane l mod 32,
 // x of lane 32 + l mod 32), the lane's own value and that of lane l ^ 32 in
 // one fixed order, so a symmetric combination of the pair is bit-identical in
