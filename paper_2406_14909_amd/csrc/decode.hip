@@ -407,8 +407,8 @@ __global__ void __launch_bounds__(kWaves * 64, 2) decode_mma_kernel(DecodeArgs a
       for (int st = 0; st < 4; ++st)
 #pragma unroll
         for (int i = 0; i < 4; ++i) tmax = fmaxf(tmax, s[st][i]);
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 16, 64));
-      tmax = fmaxf(tmax, __shfl_xor(tmax, 32, 64));
+      tmax = max_xor<16>(tmax);
+      tmax = max_xor<32>(tmax);
       const float m_new = fmaxf(m_run, tmax * c2);
       const float alpha = fast_exp2(m_run - m_new);
       m_run = m_new;
@@ -450,8 +450,8 @@ __global__ void __launch_bounds__(kWaves * 64, 2) decode_mma_kernel(DecodeArgs a
     }
 
     // Row sums of the four 16-lane groups; the running max is already shared.
-    l_run += __shfl_xor(l_run, 16, 64);
-    l_run += __shfl_xor(l_run, 32, 64);
+    l_run = sum_xor<16>(l_run);
+    l_run = sum_xor<32>(l_run);
     __syncthreads();                                // every wave is done with its V tile
     if (n < G) {
       // Lane holds O^T rows 16*dt + 4*q4 + i of query head n.

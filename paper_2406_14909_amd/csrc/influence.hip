@@ -144,7 +144,7 @@ __global__ void __launch_bounds__(INW * 64, 2) influence_kernel(InfluenceArgs a)
     float tmax = -INFINITY;
 #pragma unroll
     for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, acc.s[r]);
-    tmax = max_halves(tmax);
+    tmax = max_xor<32>(tmax);
     const float mr_new = fmaxf(mr, tmax);
     const float m_new = mr_new * c2;              // scale > 0: the scaled maximum
     const float alpha = fast_exp2(mr * c2 - m_new);
@@ -302,8 +302,8 @@ __global__ void __launch_bounds__(INW * 64, 2) influence_kernel(InfluenceArgs a)
     };
 
     run_pass(std::false_type{});
-    l = sum_halves(l);
-    u = sum_halves(u);
+    l = sum_xor<32>(l);
+    u = sum_xor<32>(u);
     lse2 = mr * c2 + __log2f(l);
     drow = u / l;
     // 1 / A of the row's largest weight, computed exactly as the second pass

@@ -170,33 +170,41 @@ __device__ __forceinline__ void sched_fence() {
 #endif
 }
 
-// The two halves of a wave exchanged: lane l gets (x of lane l mod 32,
-// x of lane 32 + l mod 32), the lane's own value and that of lane l ^ 32 in
-// one fixed order, so a symmetric combination of the pair is bit-identical in
-// both halves.  One v_permlane32_swap (a vector-ALU exchange of the halves)
-// replaces an LDS permute, whose wait would also wait for every LDS read
-// issued before it.  Checked on gfx950: with both operands holding x the
-// instruction leaves [x_0..31, x_0..31] in the first and [x_32..63,
-// x_32..63] in the second.  Written as assembly with its own wait states
-// around it; the compiler builtin for it returned its second result wrong.
-struct HalfPair {
+// Exchange with lane l ^ D (D = 32: the other half of the wave; D = 16: the
+// other row of the same pair of 16-lane rows): lane l gets its own value and
+// that of lane l ^ D in one fixed order (lower lane first), so a symmetric
+// combination of the pair is bit-identical in both lanes.  One
+// v_permlane32_swap / v_permlane16_swap (a vector-ALU exchange) replaces an
+// LDS permute, whose wait would also wait for every LDS read issued before
+// it.  Checked on gfx950: with both operands holding x, v_permlane32_swap
+// leaves [x_0..31, x_0..31] in the first and [x_32..63, x_32..63] in the
+// second; v_permlane16_swap leaves the even row of each row pair in the
+// first and the odd row in the second.  Written as assembly with its own wait
+// states around it; the compiler builtin for the 32-lane swap returned its
+// second result wrong.
+struct LanePair {
   float lo, hi;
 };
-__device__ __forceinline__ HalfPair wave_halves(float x) {
+template <int D>
+__device__ __forceinline__ LanePair lane_pair(float x) {
+  static_assert(D == 16 || D == 32, "lane distance");
 #if defined(__HIP_DEVICE_COMPILE__)
   unsigned a = __builtin_bit_cast(unsigned, x), b = a;
-  asm("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+  if constexpr (D == 32) asm("s_nop 1\n\tv_permlane32_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
+  else asm("s_nop 1\n\tv_permlane16_swap_b32 %0, %1\n\ts_nop 1" : "+v"(a), "+v"(b));
   return {__builtin_bit_cast(float, a), __builtin_bit_cast(float, b)};
 #else
   return {x, x};
 #endif
 }
-__device__ __forceinline__ float max_halves(float x) {
-  const HalfPair p = wave_halves(x);
+template <int D>
+__device__ __forceinline__ float max_xor(float x) {
+  const LanePair p = lane_pair<D>(x);
   return fmaxf(p.lo, p.hi);
 }
-__device__ __forceinline__ float sum_halves(float x) {
-  const HalfPair p = wave_halves(x);
+template <int D>
+__device__ __forceinline__ float sum_xor(float x) {
+  const LanePair p = lane_pair<D>(x);
   return p.lo + p.hi;
 }
 

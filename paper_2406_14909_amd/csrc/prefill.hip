@@ -402,7 +402,7 @@ __global__ void __launch_bounds__(NW * 64, 2) prefill_kernel(PrefillArgs a) {
     for (int sub = 0; sub < 2; ++sub)
 #pragma unroll
       for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, sacc[sub][r]);
-    tmax = max_halves(tmax) * c2;
+    tmax = max_xor<32>(tmax) * c2;
     // Raise the exponent offset only when some row of the wave needs it.
     if (__any(tmax > m_run + kRescaleSlack)) {
       const float m_new = fmaxf(m_run, tmax);
@@ -430,7 +430,7 @@ __global__ void __launch_bounds__(NW * 64, 2) prefill_kernel(PrefillArgs a) {
           for (int e = 0; e < 8; e += 2) psum = dot2_ones(pf[sub][c][e], pf[sub][c][e + 1], psum);
         }
       }
-      psum = sum_halves(psum);
+      psum = sum_xor<32>(psum);
       l_run += psum;
 
       // O^T += V^T P^T: for each 16-key step the four d-tile accumulators are
@@ -467,7 +467,7 @@ __global__ void __launch_bounds__(NW * 64, 2) prefill_kernel(PrefillArgs a) {
           psum += p;
         }
       }
-      psum = sum_halves(psum);
+      psum = sum_xor<32>(psum);
       l_run += psum;
 #pragma unroll
       for (int dt = 0; dt < D / 32; ++dt) {
