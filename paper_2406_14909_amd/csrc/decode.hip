@@ -365,28 +365,25 @@ __global__ void __launch_bounds__(kWaves * 64, 2) decode_mma_kernel(DecodeArgs a
     const float c2 = a.scale_log2;
 
     for (int t0 = lo + wave * KT; t0 < hi; t0 += kWaves * KT) {
-      // A = K rows t0 + 16*st + n, dims 32*kk + 8*q4 .. +7 (zero past hi).
+      // A = K rows t0 + 16*st + n, dims 32*kk + 8*q4 .. +7.  Rows past hi
+      // re-read row hi - 1: every load is unconditional (no branch per load);
+      // their scores are masked to -inf below, so their weights, and with
+      // them the re-read V rows, contribute exactly 0.
+      const int last = hi - 1;
       bf16x8 kop[4][KS];
 #pragma unroll
       for (int st = 0; st < 4; ++st) {
-        const int key = t0 + 16 * st + n;
-        if (key < hi) {
-          const bf16* kr = kb + int64_t(key) * D + 8 * q4;
+        const bf16* kr = kb + int64_t(min(t0 + 16 * st + n, last)) * D + 8 * q4;
 #pragma unroll
-          for (int kk = 0; kk < KS; ++kk) kop[st][kk] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(kr + 32 * kk));
-        } else {
-#pragma unroll
-          for (int kk = 0; kk < KS; ++kk) kop[st][kk] = bf16x8{};
-        }
+        for (int kk = 0; kk < KS; ++kk) kop[st][kk] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(kr + 32 * kk));
       }
       // V tile, row-major 16-byte chunks: chunk u*64 + lane is row / CPR, chunk % CPR.
       bf16x8 vr[VLD];
 #pragma unroll
       for (int u = 0; u < VLD; ++u) {
         const int m = u * 64 + lane;
-        const int key = t0 + m / CPR;
-        vr[u] = key < hi ? __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(vb + int64_t(key) * D + (m % CPR) * 8))
-                         : bf16x8{};
+        const int key = min(t0 + m / CPR, last);
+        vr[u] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(vb + int64_t(key) * D + (m % CPR) * 8));
       }
 
       f32x4 s[4];
