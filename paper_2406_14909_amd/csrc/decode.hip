@@ -44,7 +44,12 @@ namespace moa {
 namespace {
 
 constexpr int kWaves = 4;          // waves per worker (work-group)
-constexpr int kMmaKeys = 64;       // keys per wave tile in the matrix-core loop
+// Keys per wave tile in the matrix-core loop: 32 keys (32 KB of LDS and
+// about 150 VGPRs per work-group, 3 work-groups per compute unit) for G <= 4;
+// 64 keys (2 per unit) for G = 8, whose larger partials make the extra
+// workers of the higher occupancy cost more in the merge than they gain.
+template <int G>
+constexpr int mma_keys() { return G >= 8 ? 64 : 32; }
 constexpr int kFastParts = 8;      // caches split over at most this many workers merge in one pass
 
 __device__ __forceinline__ int64_t worker_start(const DecodeArgs& a, int w) {
@@ -296,9 +301,9 @@ __device__ __forceinline__ float dot2_ones(bf16 a, bf16 b, float acc) {
 #endif
 }
 
-template <int D>
+template <int D, int KEYS>
 struct MmaTile {
-  static constexpr int KT = kMmaKeys;
+  static constexpr int KT = KEYS;
   static constexpr int KS = D / 32;           // S steps over the head dimension
   static constexpr int DT = D / 16;           // 16-row output tiles of O^T
   static constexpr int RB = D * 2;            // bytes per cache row
@@ -310,9 +315,11 @@ struct MmaTile {
 };
 
 template <int D, int G>
-__global__ void __launch_bounds__(kWaves * 64, 2) decode_mma_kernel(DecodeArgs a) {
-  using TL = MmaTile<D>;
+__global__ void __launch_bounds__(kWaves * 64, mma_keys<G>() == 32 ? 3 : 2) decode_mma_kernel(DecodeArgs a) {
+  using TL = MmaTile<D, mma_keys<G>()>;
   constexpr int KT = TL::KT, KS = TL::KS, DT = TL::DT, RB = TL::RB, CPR = TL::CPR, VLD = TL::VLD;
+  constexpr int NST = KT / 16, NKS = KT / 32;   // 16-key score tiles, 32-key PV steps per wave tile
+  static_assert(KT % 32 == 0, "whole 32-key steps");
   static_assert(G >= 1 && G <= 16, "query heads per KV head");
   static_assert(kWaves * (G * D + 2 * G) * 4 <= kWaves * KT * RB, "merge state fits the V buffers");
 
@@ -370,9 +377,9 @@ __global__ void __launch_bounds__(kWaves * 64, 2) decode_mma_kernel(DecodeArgs a
       // their scores are masked to -inf below, so their weights, and with
       // them the re-read V rows, contribute exactly 0.
       const int last = hi - 1;
-      bf16x8 kop[4][KS];
+      bf16x8 kop[NST][KS];
 #pragma unroll
-      for (int st = 0; st < 4; ++st) {
+      for (int st = 0; st < NST; ++st) {
         const bf16* kr = kb + int64_t(min(t0 + 16 * st + n, last)) * D + 8 * q4;
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk) kop[st][kk] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(kr + 32 * kk));
@@ -386,22 +393,22 @@ __global__ void __launch_bounds__(kWaves * 64, 2) decode_mma_kernel(DecodeArgs a
         vr[u] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(vb + int64_t(key) * D + (m % CPR) * 8));
       }
 
-      f32x4 s[4];
+      f32x4 s[NST];
 #pragma unroll
-      for (int st = 0; st < 4; ++st) {
+      for (int st = 0; st < NST; ++st) {
         s[st] = f32x4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk) s[st] = mma16(kop[st][kk], qop[kk], s[st]);
       }
       if (t0 + KT > hi) {
 #pragma unroll
-        for (int st = 0; st < 4; ++st)
+        for (int st = 0; st < NST; ++st)
 #pragma unroll
           for (int i = 0; i < 4; ++i) s[st][i] = (t0 + 16 * st + 4 * q4 + i < hi) ? s[st][i] : -INFINITY;
       }
       float tmax = -INFINITY;
 #pragma unroll
-      for (int st = 0; st < 4; ++st)
+      for (int st = 0; st < NST; ++st)
 #pragma unroll
         for (int i = 0; i < 4; ++i) tmax = fmaxf(tmax, s[st][i]);
       tmax = max_xor<16>(tmax);
@@ -413,11 +420,11 @@ __global__ void __launch_bounds__(kWaves * 64, 2) decode_mma_kernel(DecodeArgs a
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) oacc[dt] *= alpha;
 
-      // P^T operands of the two 32-key steps: step ks takes score tiles
+      // P^T operands of the 32-key steps: step ks takes score tiles
       // 2ks (keys 4*q4 + i) and 2ks + 1 (keys 16 + 4*q4 + i).
-      bf16x8 pop[2];
+      bf16x8 pop[NKS];
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
+      for (int ks = 0; ks < NKS; ++ks) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           pop[ks][i] = static_cast<bf16>(fast_exp2(__builtin_fmaf(s[2 * ks][i], c2, -m_new)));
@@ -435,7 +442,7 @@ __global__ void __launch_bounds__(kWaves * 64, 2) decode_mma_kernel(DecodeArgs a
         *reinterpret_cast<bf16x8*>(vs + r * RB + (((c >> 1) ^ TL::swz(r)) << 5) + ((c & 1) << 4)) = vr[u];
       }
 #pragma unroll
-      for (int ks = 0; ks < 2; ++ks) {
+      for (int ks = 0; ks < NKS; ++ks) {
 #pragma unroll
         for (int dt = 0; dt < DT; ++dt) {
           const bf16x4 v0 = read_tr(vs + rd_off[dt] + (32 * ks) * RB);
