@@ -50,7 +50,7 @@ constexpr int kWaves = 4;          // waves per worker (work-group)
 // workers of the higher occupancy cost more in the merge than they gain.
 template <int G>
 constexpr int mma_keys() { return G >= 8 ? 64 : 32; }
-constexpr int kFastParts = 8;      // caches split over at most this many workers merge in one pass
+constexpr int kFastParts = 16;     // caches split over at most this many workers merge in one pass
 
 __device__ __forceinline__ int64_t worker_start(const DecodeArgs& a, int w) {
   return int64_t(w) * a.per_worker + (int64_t(w) * a.rem) / a.workers;
