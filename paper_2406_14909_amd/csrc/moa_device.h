@@ -121,17 +121,22 @@ __device__ __forceinline__ i32x4 make_desc(const void* base, uint32_t bytes) {
 // It is issued as an opaque statement, so the compiler neither counts it as an
 // LDS write nor waits for it before unrelated LDS reads; the caller orders it
 // with s_waitcnt vmcnt and a work-group barrier before the data is read.
-// It sets M0 itself; a kernel using it must have no other M0 user whose value
-// lives across the call (the prefill and influence kernels have none: their
-// only M0 writes are these).
+// The LDS address goes in as an M0 operand, so the compiler itself sets M0
+// before the statement and keeps any use of its own intact.
+// The compiler inserts no hazard wait states around inline asm, so the
+// statement carries its own: on this GPU family a vector-memory instruction
+// must come at least 5 wait states after a vector-ALU write of an SGPR it
+// reads (the compiler may rebuild the descriptor with v_readlane right
+// before), and an LDS DMA at least 1 after a scalar write of M0.  s_nop 4 is
+// those 5 wait states.
 __device__ __forceinline__ void dma16_async(i32x4 desc, uint32_t voffset, void* lds_base) {
 #if defined(__HIP_DEVICE_COMPILE__)
   typedef __attribute__((address_space(3))) char lds_char;
   const uint32_t lds = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_char*)lds_base));
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+  asm volatile("s_nop 4\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                :
-               : "s"(lds), "v"(voffset), "s"(desc)
-               : "memory", "m0");
+               : "{m0}"(lds), "v"(voffset), "s"(desc)
+               : "memory");
 #else
   (void)desc;
   (void)voffset;
