@@ -30,6 +30,60 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+class TimingEvents:
+    """Pairs of HIP events that only time launches on a stream.
+
+    They are created with hipEventDisableSystemFence.  A default HIP event
+    performs a system-scope release when it is recorded (an L2 write-back and
+    invalidation); between the decode loop's kernels each such record left
+    about 5 us of idle GPU time, which is measurement cost and not work.
+    Elapsed times are read only after a full device synchronisation, so the
+    missing fence never matters to the reading.  The events come from the HIP
+    runtime torch has loaded, so they live on torch's streams."""
+
+    DISABLE_SYSTEM_FENCE = 0x20000000
+
+    def __init__(self, pairs: int):
+        import ctypes
+
+        self._c = ctypes
+        self._hip = ctypes.CDLL("libamdhip64.so.7", mode=os.RTLD_NOLOAD | os.RTLD_LAZY)
+        self._hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+        self._hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        self._hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self._hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.ev = []
+        for _ in range(pairs):
+            pair = (ctypes.c_void_p(), ctypes.c_void_p())
+            for e in pair:
+                self._check(self._hip.hipEventCreateWithFlags(ctypes.byref(e), self.DISABLE_SYSTEM_FENCE),
+                            "hipEventCreateWithFlags")
+            self.ev.append(pair)
+
+    @staticmethod
+    def _check(rc: int, what: str) -> None:
+        if rc != 0:
+            raise RuntimeError(f"{what} failed with HIP error {rc}")
+
+    def record(self, i: int, end: int, stream) -> None:
+        """Records the start (end=0) or end (end=1) event of pair i on a torch stream."""
+        self._check(self._hip.hipEventRecord(self.ev[i][end], self._c.c_void_p(stream.cuda_stream)),
+                    "hipEventRecord")
+
+    def ms(self, i: int) -> float:
+        """Milliseconds between pair i's events (call after torch.cuda.synchronize())."""
+        out = self._c.c_float()
+        self._check(self._hip.hipEventElapsedTime(self._c.byref(out), self.ev[i][0], self.ev[i][1]),
+                    "hipEventElapsedTime")
+        return float(out.value)
+
+    def close(self) -> None:
+        for pair in self.ev:
+            for e in pair:
+                self._hip.hipEventDestroy(e)
+        self.ev = []
+
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 
 
@@ -180,34 +234,41 @@ def main() -> int:
         t = N + i // R                                  # decode step i runs on cache set i % R
         fills = sum(min(t + 1, c) for c in caps)
         dec_bytes.append(B * fills * D * 2 * esz + 2 * B * Hq * D * esz)
-    dec_bytes_total = float(sum(dec_bytes))
 
     if args.profile_kernel:
         return profile_kernel(args, M, plan, q_pre, k_pre, v_pre, o_pre, q_dec, k_dec, v_dec, o_dec,
                               kc, vc, pos, ws, N, prefill_flops, dec_bytes[0])
 
     stream = torch.cuda.current_stream()
-    n_ev = steps_dec + 1
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in range(n_ev)]
+    # Events time an even sample of at most 16 decode calls per step: each
+    # record between two kernels still leaves the GPU idle for about 4 us, so
+    # bracketing all 256 calls would slow the step it measures.  The sample
+    # takes the middle call of each stride, so it does not give the first
+    # call after the bulk cache fill (slower by up to a quarter) 16 times its
+    # share of the average.
+    stride = max(1, steps_dec // 16)
+    timed = list(range(stride // 2, steps_dec, stride))
+    slot = {i: k + 1 for k, i in enumerate(timed)}     # event pair 0 is the prefill
+    ev = TimingEvents(len(timed) + 1)
 
     def step(record: bool):
         p = M.moa_plan(Hq, Hkv, D, s, N, wl.dtype, wl.alpha, wl.beta, flags=flags)
         if record:
-            ev[0][0].record(stream)
+            ev.record(0, 0, stream)
         M.moa_prefill(p, q_pre, k_pre, v_pre, o_pre)
         if record:
-            ev[0][1].record(stream)
+            ev.record(0, 1, stream)
         for kc_r, vc_r, pos_r in sets:
             M.moa_kv_append(p, kc_r, vc_r, pos_r, k_pre, v_pre, 0)
         for i in range(steps_dec):
             t = N + i // R
             kc_r, vc_r, pos_r = sets[i % R]
             M.moa_kv_append(p, kc_r, vc_r, pos_r, k_dec[i], v_dec[i], t)
-            if record:
-                ev[i + 1][0].record(stream)
+            if record and i in slot:
+                ev.record(slot[i], 0, stream)
             M.moa_decode(p, q_dec[i], kc_r, vc_r, t, ws, o_dec)
-            if record:
-                ev[i + 1][1].record(stream)
+            if record and i in slot:
+                ev.record(slot[i], 1, stream)
         return p
 
     for _ in range(args.warmup):
@@ -221,18 +282,20 @@ def main() -> int:
         step(True)
         torch.cuda.synchronize()
         wall.append(time.perf_counter() - t0)
-        prefill_ms.append(ev[0][0].elapsed_time(ev[0][1]))
-        decode_ms.append(sum(ev[i][0].elapsed_time(ev[i][1]) for i in range(1, n_ev)))
+        prefill_ms.append(ev.ms(0))
+        decode_ms.append(sum(ev.ms(k) for k in range(1, len(timed) + 1)))
         log(f"[bench] step {len(wall)}: {wall[-1] * 1e3:.2f} ms (prefill {prefill_ms[-1]:.3f} ms, "
-            f"decode kernels {decode_ms[-1]:.3f} ms)")
+            f"{len(timed)} timed decode calls {decode_ms[-1]:.3f} ms)")
+    ev.close()
     ms_per_step = 1e3 * float(np.mean(wall))
     pre_ms = float(np.mean(prefill_ms))
-    dec_ms = float(np.mean(decode_ms))
+    dec_ms = float(np.mean(decode_ms))              # the timed calls of one step
+    timed_bytes = float(sum(dec_bytes[i] for i in timed))
     tokens = B * steps_dec
     value = tokens / (ms_per_step / 1e3)
-    dec_gbs = dec_bytes_total / (dec_ms / 1e3) / 1e9
+    dec_gbs = timed_bytes / (dec_ms / 1e3) / 1e9
     pre_tflops = prefill_flops / (pre_ms / 1e3) / 1e12
-    dec_launch_us = 1e3 * dec_ms / steps_dec
+    dec_launch_us = 1e3 * dec_ms / len(timed)
 
     dname = "bf16" if wl.dtype == "bf16" else "float"
     dec_kernel = (f"decode_mma_kernel<{D},{group}>" if wl.dtype == "bf16" and group >= 2
@@ -266,8 +329,9 @@ def main() -> int:
             "plan_flags": [name for name, on in (("block_band", args.block_band),
                                                   ("span_includes_sinks", args.span_includes_sinks)) if on],
         },
-        "decode_only_tokens_per_s": round(tokens / (dec_ms / 1e3), 2),
+        "decode_only_tokens_per_s": round(B / (dec_launch_us / 1e6), 2),
         "decode_kernel_avg_us": round(dec_launch_us, 3),
+        "decode_calls_timed_per_step": len(timed),
         "decode_hbm_gbs": round(dec_gbs, 1),
         "prefill_ms": round(pre_ms, 4),
         "prefill_inband_tflops": round(pre_tflops, 2),
@@ -280,7 +344,7 @@ def main() -> int:
             "frac": round(dec_gbs / HBM_PEAK_GBS, 4),
             "traffic": measured_traffic(f"hbm_traffic__decode_kernel__{wl.name}.md"),
             "traffic_kernel": f"{dec_kernel} (bytes per launch)",
-            "bytes_per_launch": round(dec_bytes_total / steps_dec),
+            "bytes_per_launch": round(timed_bytes / len(timed)),
         },
         "roofline_prefill": {
             "kernel": "prefill_kernel<bf16,128>, per call",
