@@ -476,23 +476,31 @@ __global__ void __launch_bounds__(kWaves * 64, mma_keys<G>() == 32 ? 3 : 2) deco
 // ---------------------------------------------------------------------------
 // Merge of the partials of every cache split over several workers:
 // o = sum_p 2^(m_p - M) acc_p / sum_p 2^(m_p - M) l_p, M = max_p m_p.
-// One work-group per (sequence, KV head); the partials of workers w0..w1 sit
-// at consecutive slots w0 + cache .. w1 + cache.  Thread groups of TPR
-// threads (one float4 of every head's row each) take every PG-th partial, so
-// PG partial rows are read at once; the groups' sums meet in LDS.
+// One work-group per (sequence, KV head, slice of at most 2 query heads): a
+// whole group of 8 heads per work-group left a GQA merge to only B * H_kv
+// work-groups, each reading up to 16 partials of every head.  The partials of
+// workers w0..w1 sit at consecutive slots w0 + cache .. w1 + cache.  Thread
+// groups of TPR threads (one float4 of each of the slice's head rows) take
+// every PG-th partial, so PG partial rows are read at once; the groups' sums
+// meet in LDS.
 // ---------------------------------------------------------------------------
+template <int G>
+constexpr int merge_heads() { return G <= 2 ? G : 2; }   // query heads per merge work-group
+
 template <typename T, int D, int G>
 __global__ void __launch_bounds__(256) decode_combine_kernel(DecodeArgs a) {
   constexpr int PS = D + kDecodePartPad;
   constexpr int V4 = D / 4;                  // float4 per head row
-  constexpr int TPR = G * V4;                // threads per partial (all heads)
+  constexpr int HS = merge_heads<G>();       // query heads per work-group
+  constexpr int TPR = HS * V4;               // threads per partial (the slice's heads)
   constexpr int PG = 256 / TPR;              // partials read at once
   constexpr int CH = 256;                    // partials whose weights are staged at a time
   static_assert(TPR <= 256 && 256 % TPR == 0, "thread mapping");
-  __shared__ float s_w[G][CH];
-  __shared__ float s_m[G], s_inv[G];
+  __shared__ float s_w[HS][CH];
+  __shared__ float s_m[HS], s_inv[HS];
   __shared__ f32x4 s_red[256];
-  const int bg = static_cast<int>(blockIdx.x);
+  const int bg = static_cast<int>(blockIdx.x) / (G / HS);
+  const int h0 = (static_cast<int>(blockIdx.x) - bg * (G / HS)) * HS;   // first head of the slice
   const int b = bg / a.hkv, g = bg - b * a.hkv;
   if (cache_fill(a, b, g) == 0) return;
   const int64_t base = int64_t(b) * a.seq_keys + a.seg_start[g];
@@ -501,7 +509,7 @@ __global__ void __launch_bounds__(256) decode_combine_kernel(DecodeArgs a) {
   if (w0 == w1) return;                       // written directly by its worker
   const int np = w1 - w0 + 1;
   const float* part0 = a.part + (int64_t(w0) + bg) * G * PS;
-  auto at = [&](int p, int h) { return part0 + (int64_t(p) * G + h) * PS; };
+  auto at = [&](int p, int h) { return part0 + (int64_t(p) * G + h0 + h) * PS; };
 
   if (np <= kFastParts) {
     // Few partials (the common case): every thread of the first TPR loads
@@ -535,14 +543,14 @@ __global__ void __launch_bounds__(256) decode_combine_kernel(DecodeArgs a) {
       acc += xp[p] * wgt;
     }
     acc *= 1.0f / ls;
-    T* op = static_cast<T*>(a.o) + (int64_t(b) * a.hq + g * G + h) * D + 4 * d4;
+    T* op = static_cast<T*>(a.o) + (int64_t(b) * a.hq + g * G + h0 + h) * D + 4 * d4;
 #pragma unroll
     for (int e = 0; e < 4; ++e) op[e] = static_cast<T>(acc[e]);
     return;
   }
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int h = wave; h < G; h += 4) {
+  for (int h = wave; h < HS; h += 4) {
     float mx = kNegBig;
     for (int p = lane; p < np; p += 64) mx = fmaxf(mx, at(p, h)[D]);
 #pragma unroll
@@ -563,7 +571,7 @@ __global__ void __launch_bounds__(256) decode_combine_kernel(DecodeArgs a) {
   f32x4 acc = {0.0f, 0.0f, 0.0f, 0.0f};
   for (int p0 = 0; p0 < np; p0 += CH) {
     const int nc = min(CH, np - p0);
-    for (int t = threadIdx.x; t < G * CH; t += 256) {
+    for (int t = threadIdx.x; t < HS * CH; t += 256) {
       const int hh = t / CH, c = t % CH;
       s_w[hh][c] = c < nc ? fast_exp2(at(p0 + c, hh)[D] - s_m[hh]) : 0.0f;
     }
@@ -588,7 +596,7 @@ __global__ void __launch_bounds__(256) decode_combine_kernel(DecodeArgs a) {
 #pragma unroll
   for (int k = 1; k < PG; ++k) acc += s_red[k * TPR + j];
   acc *= s_inv[h];
-  T* op = static_cast<T*>(a.o) + (int64_t(b) * a.hq + g * G + h) * D + 4 * d4;
+  T* op = static_cast<T*>(a.o) + (int64_t(b) * a.hq + g * G + h0 + h) * D + 4 * d4;
 #pragma unroll
   for (int e = 0; e < 4; ++e) op[e] = static_cast<T>(acc[e]);
 }
@@ -625,7 +633,7 @@ int launch_t(DecodeArgs a, void* stream) {
                                  static_cast<hipStream_t>(stream));
   if (e != hipSuccess || workers == 1) return static_cast<int>(e);   // one worker: every cache is whole
   e = hipLaunchKernel(reinterpret_cast<const void*>(&decode_combine_kernel<T, D, G>),
-                      dim3(static_cast<unsigned>(a.batch * a.hkv)), dim3(256), args, 0,
+                      dim3(static_cast<unsigned>(a.batch * a.hkv * (G / merge_heads<G>()))), dim3(256), args, 0,
                       static_cast<hipStream_t>(stream));
   return static_cast<int>(e);
 }

@@ -264,6 +264,7 @@ DECODE_CASES = [
     ("bf16", 1, 64, 8, 128, 64, [5000, 1, 3000, 64, 700, 4999, 128, 2048], 5100, 2),  # G = 8
     ("bf16", 4, 16, 2, 64, 3, [1, 2], 5, 4),                  # G = 8, one worker for the batch
     ("bf16", 8, 8, 8, 128, 64, [3000, 17, 900, 2999, 1, 1500, 333, 2000], 3000, 2),  # many workers
+    ("bf16", 1, 16, 4, 64, 16, [30000, 5, 70000, 1], 70000, 2),  # G = 4, one cache over > 16 workers
 ]
 
 
