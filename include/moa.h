@@ -184,7 +184,9 @@ size_t moa_decode_workspace_bytes(const moa_plan_t* plan, int32_t batch);
  * workspace: device buffer of ws_bytes >= moa_decode_workspace_bytes(plan,
  * batch), 256-byte aligned, holding split-K partial results; its contents
  * need no initialisation and are meaningless after the call.  Calls that
- * share one workspace must be ordered on one stream.  Launches one kernel, or
+ * share one workspace must be ordered on one stream.  Neither o nor the
+ * workspace may overlap q, the caches or each other (MOA_ERR_INVALID_ARG).
+ * Launches one kernel, or
  * two when some head's cache spans several split-K chunks (the second merges
  * the chunks' partial results). */
 moa_status_t moa_decode(const moa_plan_t* plan, const void* q, const void* k_cache,

@@ -36,6 +36,7 @@
 //                  transposing LDS read; the key order inside each 32-key
 //                  step is permuted identically on both operands.
 #include <algorithm>
+#include <atomic>
 
 #include "moa_device.h"
 
@@ -602,16 +603,18 @@ __global__ void __launch_bounds__(256) decode_combine_kernel(DecodeArgs a) {
 }
 
 // Resident work-groups of `kernel` on the current device: compute units x
-// resident work-groups per unit (cached per device).
-int resident_groups(const void* kernel, int* cache) {
+// resident work-groups per unit (cached per device; host threads may launch
+// concurrently, and they all store the same value).
+int resident_groups(const void* kernel, std::atomic<int>* cache) {
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
-  if (cache[dev] > 0) return cache[dev];
+  const int known = cache[dev].load(std::memory_order_relaxed);
+  if (known > 0) return known;
   int cus = 0, per_cu = 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) cus = 1;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, kWaves * 64, 0) != hipSuccess) per_cu = 1;
   const int groups = std::max(1, cus) * std::max(1, per_cu);
-  cache[dev] = groups;
+  cache[dev].store(groups, std::memory_order_relaxed);
   return groups;
 }
 
@@ -621,7 +624,7 @@ int launch_t(DecodeArgs a, void* stream) {
   const void* kernel;
   if constexpr (kMma) kernel = reinterpret_cast<const void*>(&decode_mma_kernel<D, G>);
   else kernel = reinterpret_cast<const void*>(&decode_valu_kernel<T, D, G>);
-  static int group_cache[64];
+  static std::atomic<int> group_cache[64];
   int64_t workers = resident_groups(kernel, group_cache);
   workers = std::min<int64_t>(workers, (a.total + kDecodeMinKeys - 1) / kDecodeMinKeys);
   workers = std::max<int64_t>(1, std::min<int64_t>(workers, kMaxDecodeWorkers));

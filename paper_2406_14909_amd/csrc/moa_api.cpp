@@ -89,6 +89,19 @@ static bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
 
 static size_t elem_size(const moa_plan_s& p) { return p.desc.dtype == MOA_BF16 ? 2 : 4; }
 
+// Decode writes o and `ws_need` bytes of the workspace; true when either
+// overlaps another argument (or the other written buffer).
+static bool decode_overlap(const moa_plan_s& p, const void* q, const void* kc, const void* vc, const void* o,
+                           int32_t batch, const void* ws, size_t ws_need) {
+  const size_t es = elem_size(p);
+  const size_t ob = es * static_cast<size_t>(batch) * p.desc.num_q_heads * p.desc.head_dim;
+  const size_t cb = es * static_cast<size_t>(batch) * static_cast<size_t>(p.offset[p.desc.num_kv_heads]) *
+                    p.desc.head_dim;
+  return overlaps(o, ob, q, ob) || overlaps(o, ob, kc, cb) || overlaps(o, ob, vc, cb) ||
+         overlaps(o, ob, ws, ws_need) || overlaps(ws, ws_need, q, ob) || overlaps(ws, ws_need, kc, cb) ||
+         overlaps(ws, ws_need, vc, cb);
+}
+
 }  // namespace moa
 
 using namespace moa;
@@ -309,6 +322,8 @@ moa_status_t moa_decode(const moa_plan_t* plan, const void* q, const void* k_cac
                                        std::to_string(need) + " bytes)");
   if (reinterpret_cast<uintptr_t>(workspace) & 255u)
     return fail(MOA_ERR_WORKSPACE, "moa_decode: workspace must be 256-byte aligned");
+  if (decode_overlap(*plan, q, k_cache, v_cache, o, batch, workspace, need))
+    return fail(MOA_ERR_INVALID_ARG, "moa_decode: o or the workspace overlaps another argument");
   const moa_desc_t& d = plan->desc;
   int64_t seg_len[MOA_MAX_KV_HEADS];
   for (int h = 0; h < d.num_kv_heads; ++h) seg_len[h] = std::min<int64_t>(pos + 1, plan->capacity[h]);
@@ -336,6 +351,8 @@ moa_status_t moa_decode_ragged(const moa_plan_t* plan, const void* q, const void
                                        std::to_string(need) + " bytes)");
   if (reinterpret_cast<uintptr_t>(workspace) & 255u)
     return fail(MOA_ERR_WORKSPACE, "moa_decode_ragged: workspace must be 256-byte aligned");
+  if (decode_overlap(*plan, q, k_cache, v_cache, o, batch, workspace, need))
+    return fail(MOA_ERR_INVALID_ARG, "moa_decode_ragged: o or the workspace overlaps another argument");
   const moa_desc_t& d = plan->desc;
   int64_t seg_len[MOA_MAX_KV_HEADS];
   for (int h = 0; h < d.num_kv_heads; ++h) seg_len[h] = plan->capacity[h];

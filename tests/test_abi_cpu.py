@@ -178,6 +178,12 @@ def test_gpu_entry_points_validate_before_launch():
     assert lib.moa_decode(h, fake, fake, fake, fake, 2, -1, fake, need, None) == M.MOA_ERR_INVALID_ARG
     assert lib.moa_decode(h, fake, fake, fake, fake, 0, 0, fake, need, None) == M.MOA_ERR_INVALID_ARG
     assert lib.moa_decode(h, None, fake, fake, fake, 2, 0, fake, need, None) == M.MOA_ERR_INVALID_ARG
+    # Written buffers (o, workspace) may not overlap anything else.
+    q, kc, vc, ws, o = 1 << 20, 1 << 28, 1 << 29, 1 << 30, 3 << 30
+    for args in ((q, kc, vc, q + 16, ws), (q, kc, vc, kc + 4096, ws), (q, kc, vc, ws + 256, ws),
+                 (q, kc, vc, o, kc + 256), (q, kc, vc, o, q)):
+        st = lib.moa_decode(h, *args[:4], 2, 0, args[4], need, None)
+        assert st == M.MOA_ERR_INVALID_ARG and "overlap" in lib.moa_last_error().decode(), args
 
 
 def test_decode_workspace_size():
@@ -223,6 +229,9 @@ def test_ragged_entry_points_validate_before_launch():
     assert lib.moa_decode_ragged(h, fake, fake, fake, fake, None, 2, fake, need, None) == M.MOA_ERR_INVALID_ARG
     assert lib.moa_decode_ragged(h, fake, fake, fake, fake, fake, 2, fake, need - 1, None) == M.MOA_ERR_WORKSPACE
     assert lib.moa_decode_ragged(h, fake, fake, fake, fake, fake, 0, fake, need, None) == M.MOA_ERR_INVALID_ARG
+    q, kc, vc, ws = 1 << 20, 1 << 28, 1 << 29, 1 << 30
+    st = lib.moa_decode_ragged(h, q, kc, vc, q + 16, fake, 2, ws, need, None)
+    assert st == M.MOA_ERR_INVALID_ARG and "overlap" in lib.moa_last_error().decode()
 
 
 def test_influence_validates_before_launch():
