@@ -22,6 +22,8 @@ import os
 import sys
 import time
 
+import numpy as np
+
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, GB/s
 BF16_MFMA_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, TFLOP/s
 
@@ -112,6 +114,40 @@ def measured_traffic(profile: str):
     if h.hexdigest() != fields["source_sha256"]:
         return None
     return int(float(fields["traffic_bytes_per_launch"]))
+
+
+def executed_wave_tiles(n: int, w: int, s: int, block: int = 0) -> int:
+    """(32-row wave, 64-key tile) products the prefill kernel runs for one
+    query head.  Each 128-row work-group visits the sink tiles [0, ta) and
+    the band tiles [tb, tl] of its rows; each of its 32-row waves multiplies
+    a visited tile when the tile holds a visible pair of one of its rows
+    (the masked entries inside such a tile are computed too).  With block
+    (64) the band counts whole 64-token blocks, ceil(w / 64) of them."""
+    sh, W = (6, -(-w // 64)) if block else (0, w)
+
+    def band_start(i):
+        return ((i >> sh) - W + 1) << sh
+
+    def inter(lo1, hi1, lo2, hi2):          # |[lo1, hi1) & [lo2, hi2)|
+        return np.maximum(0, np.minimum(hi1, hi2) - np.maximum(lo1, lo2))
+
+    r0 = np.arange(0, n, 32, dtype=np.int64)          # each wave's first row
+    r1 = np.minimum(n, r0 + 32)
+    i0 = (r0 // 128) * 128                            # its work-group's rows
+    i1 = np.minimum(n, i0 + 128)
+    ta = (np.minimum(s, i1) + 63) // 64
+    tl = (i1 - 1) // 64
+    tb = np.maximum(ta, np.maximum(0, band_start(i0)) // 64)
+    tmax = (r1 - 1) // 64                             # causal: tile starts at or before the last row
+    t_sink = (s + 63) // 64                           # tiles starting below s
+    t_band = band_start(r0) // 64                     # tiles reaching the first row's band
+    far = np.int64(1) << 40
+    total = 0
+    for lo, hi in ((np.zeros_like(ta), ta), (tb, tl + 1)):
+        hi = np.minimum(hi, tmax + 1)
+        total += int((inter(lo, hi, 0, t_sink) + inter(lo, hi, t_band, far)
+                      - inter(np.maximum(lo, t_band), hi, 0, t_sink)).sum())
+    return total
 
 
 def visible_pairs(n: int, w: int, s: int, block: int = 0) -> int:
@@ -229,6 +265,8 @@ def main() -> int:
     # ---- algorithmic work -------------------------------------------------
     group = Hq // Hkv
     prefill_flops = 4.0 * D * B * group * sum(visible_pairs(N, w, s, block) for w in windows)
+    # matrix-core work the kernel runs, masked entries of edge tiles included
+    prefill_exec_flops = 4.0 * D * B * group * 32 * 64 * sum(executed_wave_tiles(N, w, s, block) for w in windows)
     dec_bytes = []
     for i in range(steps_dec):
         t = N + i // R                                  # decode step i runs on cache set i % R
@@ -335,6 +373,8 @@ def main() -> int:
         "decode_hbm_gbs": round(dec_gbs, 1),
         "prefill_ms": round(pre_ms, 4),
         "prefill_inband_tflops": round(pre_tflops, 2),
+        "prefill_tile_efficiency": round(prefill_flops / prefill_exec_flops, 4),
+        "prefill_executed_tflops": round(prefill_exec_flops / (pre_ms / 1e3) / 1e12, 2),
         "roofline": {
             "kernel": f"moa_decode ({dec_kernel} + decode_combine_kernel), per call",
             "bound": "hbm",
