@@ -55,56 +55,11 @@ __device__ __forceinline__ Vec16<T> load16_stream(const T* p) {
 }
 
 template <typename T>
-__device__ __forceinline__ void store16(T* p, const Vec16<T>& x) {
-  *reinterpret_cast<decltype(x.v)*>(p) = x.v;
-}
-
-template <typename T>
 __device__ __forceinline__ Vec16<T> zero16() {
   Vec16<T> r;
 #pragma unroll
   for (int i = 0; i < Vec16<T>::N; ++i) r.set(i, 0.0f);
   return r;
-}
-
-// Direct global -> LDS copy of 16 bytes per lane (gfx950 global_load_lds_dwordx4):
-// lane i's bytes land at lds_base + 16 * i; lds_base must be wave-uniform.
-// The builtin is emitted only in the device pass (the host pass just needs the
-// kernel stubs and would otherwise drop some instantiations).
-__device__ __forceinline__ void dma16(const void* src, void* lds_base) {
-#if defined(__HIP_DEVICE_COMPILE__)
-  __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)lds_base, 16, 0, 0);
-#else
-  (void)src;
-  (void)lds_base;
-#endif
-}
-
-// Buffer resource over [base, base + bytes): loads at offsets past `bytes`
-// return zeros instead of touching memory (raw addressing, gfx9-family
-// descriptor word 3).
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
-#if defined(__HIP_DEVICE_COMPILE__)
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
-#else
-  (void)base;
-  (void)bytes;
-  __amdgpu_buffer_rsrc_t r;
-  return r;
-#endif
-}
-
-// 16 bytes per lane from a buffer (at byte offset `voffset`) straight into LDS:
-// lane i's bytes land at lds_base + 16 * i; lds_base must be wave-uniform.
-__device__ __forceinline__ void dma16_buf(__amdgpu_buffer_rsrc_t rsrc, uint32_t voffset, void* lds_base) {
-#if defined(__HIP_DEVICE_COMPILE__)
-  __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)lds_base, 16,
-                                           voffset, 0, 0, 0);
-#else
-  (void)rsrc;
-  (void)voffset;
-  (void)lds_base;
-#endif
 }
 
 // Raw buffer descriptor (4 dwords, wave-uniform) over [base, base + bytes),
