@@ -15,8 +15,9 @@
  *                  the sinks and the latest window tokens, replacing the
  *                  oldest non-sink entry in place (paper Appendix
  *                  "Efficiency Experiment Setup", "Memory and Throughput
- *                  Breakdown": the cache length equals the span and old
- *                  entries beyond it are replaced by the latest).
+ *                  Breakdown": a head's cache is exactly as long as its
+ *                  span, and a new token overwrites the entry that has
+ *                  left the span).
  *   moa_decode     one query token per sequence against the per-head caches
  *                  of different lengths (paper Appendix "Efficiency
  *                  Experiment Setup": decode over KV caches whose length
@@ -161,7 +162,7 @@ moa_status_t moa_prefill(const moa_plan_t* plan, const void* q, const void* k, c
 
 /* Appends positions start_pos .. start_pos + n_new - 1 of every sequence to
  * the per-head static caches (paper Appendix "Efficiency Experiment Setup":
- * the oldest KV entry beyond the span is replaced by the latest).  k_new,
+ * a new token takes the slot of the entry that has just left the span).  k_new,
  * v_new: device [batch, n_new, num_kv_heads, head_dim].  Only each slot's
  * final occupant is written (K/V bits copied exactly, pos_cache set to the
  * position), so one bulk append equals n_new single appends.  Protocol:

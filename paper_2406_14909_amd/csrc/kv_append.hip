@@ -1,7 +1,7 @@
 // Static per-head KV cache append with in-place replacement of the oldest
-// non-sink entry (paper Appendix "Efficiency Experiment Setup": the cache
-// holds each head's span and old entries beyond it are replaced by the
-// latest).  Slot of position p: p if p < s, else s + ((p - s) mod w_g).
+// non-sink entry (paper Appendix "Efficiency Experiment Setup": each head's
+// cache is as long as its span, and a new token overwrites the entry that has
+// left it).  Slot of position p: p if p < s, else s + ((p - s) mod w_g).
 //
 // Only each slot's final occupant among the appended positions is written,
 // so a bulk (prefill) append touches at most C_g rows per head and equals
