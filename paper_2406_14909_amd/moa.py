@@ -181,6 +181,16 @@ def _stream(t, stream) -> ctypes.c_void_p:
     return ctypes.c_void_p(stream.cuda_stream)
 
 
+def _one_device(**tensors):
+    """The GPU that every tensor of a call lives on; the call runs with it as
+    the current device (raises if the tensors are spread over devices)."""
+    devs = {t.device for t in tensors.values()}
+    if len(devs) != 1:
+        raise MoaError(MOA_ERR_INVALID_ARG, "tensors on different devices: " +
+                       ", ".join(f"{k} on {t.device}" for k, t in tensors.items()))
+    return devs.pop()
+
+
 def _need(t, shape, dtype, name):
     if tuple(t.shape) != tuple(shape):
         raise MoaError(MOA_ERR_INVALID_ARG, f"{name}: expected shape {tuple(shape)}, got {tuple(t.shape)}")
@@ -203,8 +213,9 @@ def moa_prefill(plan: Plan, q, k, v, o=None, stream=None):
     if o is None:
         o = torch.empty_like(q)
     _need(o, q.shape, dt, "o")
-    _check(load_library().moa_prefill(plan.handle, q.data_ptr(), k.data_ptr(), v.data_ptr(),
-                                      o.data_ptr(), bsz, n, _stream(q, stream)))
+    with torch.cuda.device(_one_device(q=q, k=k, v=v, o=o)):
+        _check(load_library().moa_prefill(plan.handle, q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                                          o.data_ptr(), bsz, n, _stream(q, stream)))
     return o
 
 
@@ -229,9 +240,10 @@ def moa_kv_append(plan: Plan, k_cache, v_cache, pos_cache, k_new, v_new, start_p
     _need(k_cache, (bsz, plan.cache_rows, plan.head_dim), dt, "k_cache")
     _need(v_cache, (bsz, plan.cache_rows, plan.head_dim), dt, "v_cache")
     _need(pos_cache, (bsz, plan.cache_rows), torch.int32, "pos_cache")
-    _check(load_library().moa_kv_append(plan.handle, k_cache.data_ptr(), v_cache.data_ptr(),
-                                        pos_cache.data_ptr(), k_new.data_ptr(), v_new.data_ptr(),
-                                        bsz, int(start_pos), n_new, _stream(k_new, stream)))
+    with torch.cuda.device(_one_device(k_cache=k_cache, v_cache=v_cache, pos_cache=pos_cache, k_new=k_new, v_new=v_new)):
+        _check(load_library().moa_kv_append(plan.handle, k_cache.data_ptr(), v_cache.data_ptr(),
+                                            pos_cache.data_ptr(), k_new.data_ptr(), v_new.data_ptr(),
+                                            bsz, int(start_pos), n_new, _stream(k_new, stream)))
 
 
 def moa_decode_workspace_bytes(plan: Plan, batch: int) -> int:
@@ -259,9 +271,10 @@ def moa_decode(plan: Plan, q, k_cache, v_cache, pos: int, workspace, o=None, str
     if workspace.device.type != "cuda" or not workspace.is_contiguous():
         raise MoaError(MOA_ERR_WORKSPACE, "workspace must be a contiguous GPU tensor")
     nbytes = workspace.numel() * workspace.element_size()
-    _check(load_library().moa_decode(plan.handle, q.data_ptr(), k_cache.data_ptr(),
-                                     v_cache.data_ptr(), o.data_ptr(), bsz, int(pos),
-                                     workspace.data_ptr(), nbytes, _stream(q, stream)))
+    with torch.cuda.device(_one_device(q=q, k_cache=k_cache, v_cache=v_cache, o=o, workspace=workspace)):
+        _check(load_library().moa_decode(plan.handle, q.data_ptr(), k_cache.data_ptr(),
+                                         v_cache.data_ptr(), o.data_ptr(), bsz, int(pos),
+                                         workspace.data_ptr(), nbytes, _stream(q, stream)))
     return o
 
 
@@ -285,9 +298,10 @@ def moa_kv_append_ragged(plan: Plan, k_cache, v_cache, pos_cache, k_new, v_new, 
     _need(v_cache, (bsz, plan.cache_rows, plan.head_dim), dt, "v_cache")
     _need(pos_cache, (bsz, plan.cache_rows), torch.int32, "pos_cache")
     _positions(positions, bsz)
-    _check(load_library().moa_kv_append_ragged(plan.handle, k_cache.data_ptr(), v_cache.data_ptr(),
-                                               pos_cache.data_ptr(), k_new.data_ptr(), v_new.data_ptr(),
-                                               positions.data_ptr(), bsz, _stream(k_new, stream)))
+    with torch.cuda.device(_one_device(k_cache=k_cache, v_cache=v_cache, pos_cache=pos_cache, k_new=k_new, v_new=v_new, positions=positions)):
+        _check(load_library().moa_kv_append_ragged(plan.handle, k_cache.data_ptr(), v_cache.data_ptr(),
+                                                   pos_cache.data_ptr(), k_new.data_ptr(), v_new.data_ptr(),
+                                                   positions.data_ptr(), bsz, _stream(k_new, stream)))
 
 
 def moa_decode_ragged(plan: Plan, q, k_cache, v_cache, positions, workspace, o=None, stream=None):
@@ -305,9 +319,10 @@ def moa_decode_ragged(plan: Plan, q, k_cache, v_cache, positions, workspace, o=N
     if workspace.device.type != "cuda" or not workspace.is_contiguous():
         raise MoaError(MOA_ERR_WORKSPACE, "workspace must be a contiguous GPU tensor")
     nbytes = workspace.numel() * workspace.element_size()
-    _check(load_library().moa_decode_ragged(plan.handle, q.data_ptr(), k_cache.data_ptr(),
-                                            v_cache.data_ptr(), o.data_ptr(), positions.data_ptr(), bsz,
-                                            workspace.data_ptr(), nbytes, _stream(q, stream)))
+    with torch.cuda.device(_one_device(q=q, k_cache=k_cache, v_cache=v_cache, o=o, positions=positions, workspace=workspace)):
+        _check(load_library().moa_decode_ragged(plan.handle, q.data_ptr(), k_cache.data_ptr(),
+                                                v_cache.data_ptr(), o.data_ptr(), positions.data_ptr(), bsz,
+                                                workspace.data_ptr(), nbytes, _stream(q, stream)))
     return o
 
 
@@ -327,8 +342,9 @@ def moa_influence(q, k, v, dout, ebar=None, softmax_scale: float = 0.0, stream=N
         ebar = torch.empty((hq, nb, nb), dtype=torch.float32, device=q.device)
     _need(ebar, (hq, nb, nb), torch.float32, "ebar")
     desc = moa_desc_t(hq, hkv, d, 0, n, MOA_BF16, float(softmax_scale), 0, 0)
-    _check(load_library().moa_influence(ctypes.byref(desc), q.data_ptr(), k.data_ptr(), v.data_ptr(),
-                                        dout.data_ptr(), ebar.data_ptr(), bsz, n, _stream(q, stream)))
+    with torch.cuda.device(_one_device(q=q, k=k, v=v, dout=dout, ebar=ebar)):
+        _check(load_library().moa_influence(ctypes.byref(desc), q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                                            dout.data_ptr(), ebar.data_ptr(), bsz, n, _stream(q, stream)))
     return ebar
 
 
@@ -347,9 +363,10 @@ def moa_rule_loss(ebar, n: int, num_sink: int, alpha, beta, flags: int = 0, stre
     r = int(a.shape[0])
     dl = torch.empty((h, r), dtype=torch.float64, device=ebar.device)
     dens = torch.empty((r,), dtype=torch.float64, device=ebar.device)
-    _check(load_library().moa_rule_loss(ebar.data_ptr(), h, int(n), int(num_sink), int(flags),
-                                        a.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
-                                        b.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), r,
-                                        dl.data_ptr(), dens.data_ptr(), _stream(ebar, stream)))
+    with torch.cuda.device(_one_device(ebar=ebar, dl=dl, density=dens)):
+        _check(load_library().moa_rule_loss(ebar.data_ptr(), h, int(n), int(num_sink), int(flags),
+                                            a.ctypes.data_as(ctypes.POINTER(ctypes.c_double)),
+                                            b.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), r,
+                                            dl.data_ptr(), dens.data_ptr(), _stream(ebar, stream)))
     return dl, dens
 

@@ -250,3 +250,12 @@ def test_influence_validates_before_launch():
     assert call(ebar=fake + 2) == M.MOA_ERR_INVALID_ARG
     assert "moa_influence" in lib.moa_last_error().decode()
 
+
+
+def test_binding_rejects_tensors_on_different_devices():
+    import torch
+    a, b = torch.zeros(4), torch.zeros(4, device="meta")
+    with pytest.raises(M.MoaError) as e:
+        M._one_device(q=a, k=b)
+    assert "different devices" in str(e.value)
+    assert M._one_device(q=a, k=torch.ones(2)) == a.device
