@@ -242,8 +242,10 @@ moa_status_t moa_influence(const moa_desc_t* desc, const void* q, const void* k,
  *   dl[h][r] = sum over i, j with j <= i of M_r(i, j) * ebar[h][i / 64][j / 64],
  * M_r(i, j) = 1 iff rule r's mask (window from (alpha[r], beta[r]) at length n
  * exactly as moa_plan evaluates it under `flags`, num_sink sinks, token or
- * MOA_BLOCK_BAND band) hides key j from query i.  density[r] = fraction of the
- * n (n + 1) / 2 causal pairs rule r keeps.
+ * MOA_BLOCK_BAND band) hides key j from query i.  density[r] is rule r's
+ * in-memory KV-cache length over the sequence length during decoding (paper
+ * Sec. 4 "Setups"): min(num_sink + w_r, n) / n, the share of the n tokens
+ * that its token-exact cache holds (the block band does not change it).
  * ebar   fp32 device [num_heads, nb, nb], nb = ceil(n / 64) (moa_influence output)
  * dl     fp64 device [num_heads, num_rules];  density fp64 device [num_rules]
  * alpha, beta: host arrays of num_rules finite doubles; 1 <= num_rules <= 64;

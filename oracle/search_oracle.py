@@ -14,7 +14,13 @@ What it computes, in the paper's terms:
   E_bar is block-averaged, so every token (i, j) of a block carries the
   block's value.  M_r marks the causal pairs (j <= i) that the rule's mask
   hides: the rule's window (and sinks, block band) from the plan's reading.
-* Density of a rule at length N: the fraction of the causal pairs it keeps.
+* Density of a rule at length N (Sec. 4 "Setups": the average in-memory
+  KV-cache length divided by the sequence length during decoding): the
+  number of tokens the rule's cache holds once N tokens have been seen,
+  divided by N.  The cache then holds exactly the keys the newest token sees
+  (the token-exact visible set of query N - 1: the sinks and the last w
+  tokens), so the density is |J_{N-1}| / N.  The block band changes only the
+  prefill mask, not the cache, so it does not enter the density.
 * Single-length selection (Appendix "Optimizing at Single Length"): choose
   one rule per head minimising the mean loss subject to the mean density
   not exceeding the budget; optionally at most K distinct rules per layer.
@@ -23,10 +29,10 @@ What it computes, in the paper's terms:
   the Pareto front of the per-length mean losses over all assignments that
   meet every length's density budget, by enumeration.
 
-Parity status: pinned by the CPU tests (a hand-worked masked sum, the
-loss / density identity under a unit profile, hand-worked selection and
-Pareto examples, enumeration checked against a library MILP solver);
-nothing is unpinned.
+Parity status: pinned by the CPU tests (a hand-worked masked sum and
+density, the masked-pair count under a unit profile, the density against a
+simulated cache, hand-worked selection and Pareto examples, enumeration
+checked against a library MILP solver); nothing is unpinned.
 """
 from __future__ import annotations
 
@@ -35,7 +41,7 @@ from typing import Optional, Sequence
 
 import numpy as np
 
-from .moa_oracle import visible_mask, window_ref
+from .moa_oracle import visible_mask, visible_set, window_ref
 
 
 def candidate_rules(n_alpha: int = 6, n_beta: int = 9):
@@ -58,19 +64,27 @@ def rule_loss_ref(ebar: np.ndarray, n: int, num_sink: int, alpha: Sequence[float
 
     ebar: [H, nb, nb] block-averaged influence (profile_block x profile_block
     blocks); each token pair takes its block's value (Eq. 4 summed token by
-    token)."""
+    token).  density[r] = |cache of rule r after n tokens| / n (Sec. 4
+    "Setups"), see density_ref."""
     ebar = np.asarray(ebar, dtype=np.float64)
     h = ebar.shape[0]
     tok = np.repeat(np.repeat(ebar, profile_block, axis=1), profile_block, axis=2)[:, :n, :n]
-    causal_count = n * (n + 1) // 2
     dl = np.zeros((h, len(alpha)), dtype=np.float64)
     dens = np.zeros(len(alpha), dtype=np.float64)
     for r, (a, b) in enumerate(zip(alpha, beta)):
         w = window_ref(a, b, n, num_sink, span_includes_sinks)
         m = masked_pairs(n, w, num_sink, block)
         dl[:, r] = (tok * m[None]).sum(axis=(1, 2))
-        dens[r] = (causal_count - int(m.sum())) / causal_count
+        dens[r] = density_ref(n, w, num_sink)
     return dl, dens
+
+
+def density_ref(n: int, w: int, s: int) -> float:
+    """Density of a head with window w and s sinks at sequence length n
+    (Sec. 4 "Setups": in-memory KV-cache length / sequence length, during
+    decoding).  After n tokens the cache holds the token-exact visible set of
+    the newest token, J_{n-1} (the sinks and the last w tokens)."""
+    return len(visible_set(n - 1, w, s)) / n
 
 
 def select_bruteforce(dl: np.ndarray, density: np.ndarray, budget: float,

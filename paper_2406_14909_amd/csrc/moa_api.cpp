@@ -441,6 +441,8 @@ moa_status_t moa_rule_loss(const float* ebar, int32_t num_heads, int64_t n, int3
   for (int r = 0; r < num_rules; ++r) {
     const int64_t w = rule_window(alpha[r], beta[r], n, num_sink, flags);
     a.window[r] = static_cast<int32_t>((flags & MOA_BLOCK_BAND) ? (w + MOA_BAND_BLOCK - 1) / MOA_BAND_BLOCK : w);
+    // the token-exact cache holds the sinks and the last w tokens (at most n)
+    a.kv_len[r] = static_cast<int32_t>(std::min<int64_t>(int64_t(num_sink) + w, n));
   }
   const int err = launch_rule_loss(a, hip_stream);
   if (err) return fail(MOA_ERR_HIP, "moa_rule_loss: kernel launch failed (hipError " + std::to_string(err) + ")");

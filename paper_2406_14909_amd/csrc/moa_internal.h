@@ -128,6 +128,7 @@ struct RuleLossArgs {
   int32_t num_sink;
   int32_t band_shift;        // 0: token band; 6: band in 64-token blocks
   int32_t window[kMaxRules]; // per rule: band length in units of 2^band_shift tokens
+  int32_t kv_len[kMaxRules]; // per rule: tokens its cache holds at length n, min(s + w, n)
 };
 
 // Kernel launchers (return hipError_t as int; 0 = success).

@@ -8,7 +8,9 @@
 // form: with the block band the band start is constant over the block's rows;
 // with the token band it moves by one per row, and the row sum is an
 // arithmetic series clipped to [0, block width].  Also writes each rule's
-// density, the fraction of causal pairs it keeps.
+// density (paper Sec. 4 "Setups": in-memory KV-cache length over sequence
+// length during decoding), kv_len / n, with kv_len = min(s + w, n) the tokens
+// the rule's token-exact cache holds once n tokens have been seen.
 //
 // One work-group per head; lane r of every wave handles rule r; the 4 waves
 // take interleaved block rows and meet in LDS.  Sums are fp64.
@@ -87,7 +89,6 @@ __global__ void __launch_bounds__(kWaves * 64) rule_loss_kernel(RuleLossArgs a) 
   __shared__ double s_pre[kWaves][kChunks * 64];     // prefix sums of one row per wave
   __shared__ float s_raw[kWaves][kChunks * 64];      // the row itself
   __shared__ double s_dl[kWaves][kMaxRules];
-  __shared__ double s_mask[kWaves][kMaxRules];
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int h = static_cast<int>(blockIdx.x);
@@ -99,8 +100,7 @@ __global__ void __launch_bounds__(kWaves * 64) rule_loss_kernel(RuleLossArgs a) 
   float* raw = s_raw[wave];
   const int ja = (s + kBlock - 1) / kBlock;                  // first block with no sink column
   const int js = (s % kBlock) ? s / kBlock : -1;             // block holding the sink edge, if any
-  const bool count_pairs = h == 0;                           // densities: one work-group counts
-  double acc = 0.0, masked = 0.0;
+  double acc = 0.0;
 
   // The wave's rows I = wave + kWaves * k are processed in groups of kDepth;
   // the next group is loaded into registers (lane holds J = 64 c + lane)
@@ -144,7 +144,6 @@ __global__ void __launch_bounds__(kWaves * 64) rule_loss_kernel(RuleLossArgs a) 
     if (jb >= ja) {
       const double lo = ja > 0 ? pre[ja - 1] : 0.0;
       acc += static_cast<double>(rows) * (pre[jb] - lo);
-      if (count_pairs) masked += static_cast<double>(rows) * static_cast<double>(min((jb + 1) * kBlock, n) - ja * kBlock);
     }
     // blocks masked in part: the block holding the sink edge, and with the
     // token band the two blocks the band start sweeps across this row block
@@ -156,7 +155,6 @@ __global__ void __launch_bounds__(kWaves * 64) rule_loss_kernel(RuleLossArgs a) 
       if (c > 0 && J == js) continue;
       const int cnt = masked_in_block(I, J, n, s, w, a.band_shift);
       acc += static_cast<double>(cnt) * static_cast<double>(raw[J]);
-      if (count_pairs) masked += static_cast<double>(cnt);
     }
   };
   float cur[kDepth][kChunks], nxt[kDepth][kChunks];
@@ -174,20 +172,13 @@ __global__ void __launch_bounds__(kWaves * 64) rule_loss_kernel(RuleLossArgs a) 
       for (int c = 0; c < kChunks; ++c) cur[d][c] = nxt[d][c];
   }
   s_dl[wave][lane] = acc;
-  s_mask[wave][lane] = masked;
   __syncthreads();
   if (wave != 0 || !rule_ok) return;
-  double dl = 0.0, mk = 0.0;
+  double dl = 0.0;
 #pragma unroll
-  for (int v = 0; v < kWaves; ++v) {
-    dl += s_dl[v][lane];
-    mk += s_mask[v][lane];
-  }
+  for (int v = 0; v < kWaves; ++v) dl += s_dl[v][lane];
   a.dl[int64_t(h) * a.num_rules + lane] = dl;
-  if (h == 0) {
-    const double causal = 0.5 * static_cast<double>(n) * (static_cast<double>(n) + 1.0);
-    a.density[lane] = (causal - mk) / causal;
-  }
+  if (h == 0) a.density[lane] = static_cast<double>(a.kv_len[lane]) / static_cast<double>(n);
 }
 
 }  // namespace

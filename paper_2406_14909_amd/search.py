@@ -34,7 +34,9 @@ def candidate_rules(n_alpha: int = 6, n_beta: int = 9) -> Tuple[np.ndarray, np.n
 def select_rules(dl, density, budget: float, layer_of: Optional[Sequence[int]] = None,
                  max_rules_per_layer: int = 0, time_limit: float = 60.0):
     """Exact single-length selection.  dl: [H, R] losses; density: [R] (or
-    [H, R]) kept fractions.  Returns (rules [H] ints, mean loss), or
+    [H, R]) rule densities (in-memory KV-cache length over sequence length,
+    paper Sec. 4 "Setups", as moa_rule_loss returns them).  Returns
+    (rules [H] ints, mean loss), or
     (None, inf) when no assignment meets the budget."""
     return _solve(dl, [(density, -np.inf, budget)], layer_of, max_rules_per_layer, time_limit)
 
@@ -102,7 +104,7 @@ def select_multi_length(dls, densities, budgets, intervals: int = 5, val_dl=None
     method (paper Appendix "Optimizing at Multiple Lengths").
 
     dls: per profiled length, the [H, R] loss table; densities: per length,
-    the [R] kept fractions; budgets: per length, the mean-density budget (None:
+    the [R] rule densities; budgets: per length, the mean-density budget (None:
     no constraint at that length).  First each length's loss is minimised
     alone, recording the other lengths' losses, which gives each length a loss
     range; then, for each length, its loss is minimised again with every other

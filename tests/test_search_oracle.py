@@ -26,18 +26,60 @@ def test_candidate_rule_grid():
     assert sorted(set(b)) == [k / 8 for k in range(9)]
 
 
+def _masked_count(n, w, s, block):
+    """Causal pairs hidden by window w and s sinks, by brute force over (i, j)."""
+    nbw = -(-w // block) if block else 0
+    count = 0
+    for i in range(n):
+        for j in range(i + 1):
+            if j < s:
+                continue
+            in_band = (i // block - j // block < nbw) if block else (i - j < w)
+            count += not in_band
+    return count
+
+
 @pytest.mark.parametrize("block", [0, 4])
 def test_unit_profile_counts_masked_pairs(block):
     # With E_bar = 1 on and below the diagonal blocks, Delta L is the number of
-    # masked causal pairs, i.e. (1 - density) * N (N + 1) / 2.
+    # masked causal pairs.
     n = 21
     nb = -(-n // 4)
     ebar = np.tril(np.ones((nb, nb)))[None]
     a, b = so.candidate_rules()
     a = a / 512.0   # small windows at this length
     dl, dens = so.rule_loss_ref(ebar, n, 2, a, b, span_includes_sinks=True, block=block, profile_block=4)
-    np.testing.assert_allclose(dl[0], (1.0 - dens) * n * (n + 1) / 2, rtol=0, atol=1e-9)
+    for r in range(len(a)):
+        w = so.window_ref(a[r], b[r], n, 2, True)
+        assert dl[0, r] == _masked_count(n, w, 2, block)
     assert np.all((dens > 0) & (dens <= 1))
+
+
+@pytest.mark.parametrize("n, s", [(1, 0), (7, 0), (7, 3), (20, 4), (33, 40)])
+def test_density_is_cache_length_over_n(n, s):
+    # Density (Sec. 4 "Setups"): in-memory KV-cache length / sequence length
+    # during decoding.  Simulate the cache (fill in arrival order, then replace
+    # the oldest non-sink entry) over n tokens and count what it holds; the
+    # block band leaves the cache token-exact, so it does not change density.
+    from oracle.moa_oracle import CacheModel
+    for w in range(1, n + 1):
+        cm = CacheModel(w, s)
+        for p in range(n):
+            cm.append(p)
+        held = len(cm.positions())
+        assert so.density_ref(n, w, s) == held / n
+        assert held == min(n, s + w)
+        for block in (0, 4):
+            _, d = so.rule_loss_ref(np.zeros((1, 9, 9)), n, s, [float(w)], [0.0], block=block, profile_block=4)
+            assert d[0] == held / n
+
+
+def test_density_half_band_rule():
+    # A plain band w = N/2 with no sinks keeps half the sequence in memory:
+    # density 0.5 (the kept share of the causal pairs would be about 3/4).
+    n = 64
+    _, d = so.rule_loss_ref(np.zeros((1, 1, 1)), n, 0, [32.0], [0.0])
+    assert d[0] == 0.5
 
 
 def test_selection_hand_example():
