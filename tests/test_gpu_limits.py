@@ -6,7 +6,7 @@ import torch
 
 import oracle
 import workloads
-from helpers import assert_close, bits
+from helpers import assert_close, bits, oracle_windows
 from oracle import influence_oracle as io
 from paper_2406_14909_amd import moa as M
 
@@ -24,6 +24,7 @@ def test_max_heads_prefill_append_decode():
     windows = [int(x) for x in rng.integers(1, n + 1, hkv)]
     windows[:4] = [1, 64, 65, n]
     plan = M.moa_plan(hq, hkv, d, s, n, "bf16", [float(w) for w in windows], [0.0] * hkv)
+    rw = oracle_windows(plan, windows, [0.0] * hkv)
     q = workloads.randn((bsz, n + 1, hq, d), 900, torch.bfloat16, "cuda")
     k = workloads.randn((bsz, n + 1, hkv, d), 901, torch.bfloat16, "cuda")
     v = workloads.randn((bsz, n + 1, hkv, d), 902, torch.bfloat16, "cuda")
@@ -34,11 +35,11 @@ def test_max_heads_prefill_append_decode():
     M.moa_kv_append(plan, kc, vc, pos, k[:, n:].contiguous(), v[:, n:].contiguous(), n)
     od = M.moa_decode(plan, q[:, n].contiguous(), kc, vc, n, ws)
     torch.cuda.synchronize()
-    assert_close(o, oracle.attention_ref(q[:, :n], k[:, :n], v[:, :n], plan.window, s), torch.bfloat16,
+    assert_close(o, oracle.attention_ref(q[:, :n], k[:, :n], v[:, :n], rw, s), torch.bfloat16,
                  with_rounding=True, what="prefill 512/64 heads")
-    assert_close(od, oracle.decode_ref(q[:, n], k, v, plan.window, s), torch.bfloat16, with_rounding=True,
+    assert_close(od, oracle.decode_ref(q[:, n], k, v, rw, s), torch.bfloat16, with_rounding=True,
                  what="decode 512/64 heads")
-    epos, ek, ev = oracle.cache_contents_ref(k.cpu(), v.cpu(), plan.window, s)
+    epos, ek, ev = oracle.cache_contents_ref(k.cpu(), v.cpu(), rw, s)
     assert np.array_equal(pos.cpu().numpy(), epos)
     assert torch.equal(bits(kc), bits(ek)) and torch.equal(bits(vc), bits(ev))
     # influence profile at the same head counts (dense attention)
@@ -55,6 +56,7 @@ def test_large_batch_append_and_decode():
     bsz, hq, hkv, d, s, n0 = 4096, 4, 2, 64, 2, 20
     _say("batch", bsz)
     plan = M.moa_plan(hq, hkv, d, s, n0, "bf16", [8.0, 16.0], [0.0, 0.0])
+    rw = oracle_windows(plan, [8.0, 16.0], [0.0, 0.0])
     k = workloads.randn((bsz, n0 + 1, hkv, d), 910, torch.bfloat16, "cuda")
     v = workloads.randn((bsz, n0 + 1, hkv, d), 911, torch.bfloat16, "cuda")
     q = workloads.randn((bsz, hq, d), 912, torch.bfloat16, "cuda")
@@ -65,8 +67,8 @@ def test_large_batch_append_and_decode():
     od = M.moa_decode(plan, q, kc, vc, n0, ws)
     torch.cuda.synchronize()
     sample = [0, 1, 777, 2048, 4095]
-    ref = oracle.decode_ref(q[sample], k[sample], v[sample], plan.window, s)
+    ref = oracle.decode_ref(q[sample], k[sample], v[sample], rw, s)
     assert_close(od[sample], ref, torch.bfloat16, with_rounding=True, what="decode B=4096")
-    epos, ek, ev = oracle.cache_contents_ref(k[sample].cpu(), v[sample].cpu(), plan.window, s)
+    epos, ek, ev = oracle.cache_contents_ref(k[sample].cpu(), v[sample].cpu(), rw, s)
     assert np.array_equal(pos[sample].cpu().numpy(), epos)
     assert torch.equal(bits(kc[sample]), bits(ek)) and torch.equal(bits(vc[sample]), bits(ev))

@@ -9,7 +9,7 @@ import torch
 
 import oracle
 import workloads
-from helpers import BF16_ATOL, assert_close, bits, guard_intact, guarded_empty
+from helpers import BF16_ATOL, F32_ATOL, assert_close, bits, guard_intact, guarded_empty, oracle_windows
 from paper_2406_14909_amd import moa as M
 
 pytestmark = pytest.mark.gpu
@@ -28,8 +28,12 @@ def _inputs(bsz, n, hq, hkv, d, dtype, seed):
     return q, k, v
 
 
-def _plan(hq, hkv, d, s, n, dtype, windows):
-    return M.moa_plan(hq, hkv, d, s, n, dtype, [float(w) for w in windows], [0.0] * len(windows))
+def _plan(hq, hkv, d, s, n, dtype, windows, flags=0):
+    """Plan with rule alpha = w, beta = 0 per head, and the oracle's windows
+    for the same rule (what every oracle call below is given)."""
+    alpha, beta = [float(w) for w in windows], [0.0] * len(windows)
+    plan = M.moa_plan(hq, hkv, d, s, n, dtype, alpha, beta, flags=flags)
+    return plan, oracle_windows(plan, alpha, beta, bool(flags & M.MOA_SPAN_INCLUDES_SINKS))
 
 
 # ---------------------------------------------------------------------------
@@ -55,13 +59,13 @@ def test_prefill_matches_oracle(case):
     dt, bsz, n, hq, hkv, d, s, windows = case
     _say("prefill", case)
     dtype = DT[dt]
-    plan = _plan(hq, hkv, d, s, n, dt, windows)
+    plan, rw = _plan(hq, hkv, d, s, n, dt, windows)
     q, k, v = _inputs(bsz, n, hq, hkv, d, dtype, 100 + n)
     o, buf = guarded_empty(q.shape, dtype)
     M.moa_prefill(plan, q, k, v, o)
     torch.cuda.synchronize()
     assert guard_intact(buf, q.shape), "write past the output"
-    ref = oracle.attention_ref(q, k, v, plan.window, s)
+    ref = oracle.attention_ref(q, k, v, rw, s)
     assert_close(o, ref, dtype, with_rounding=True, what=f"prefill {case}")
 
 
@@ -70,7 +74,7 @@ def test_prefill_window_one_no_sink_is_identity(dt):
     _say("prefill w=1 s=0", dt)
     dtype = DT[dt]
     bsz, n, hq, hkv, d = 2, 389, 8, 4, 128
-    plan = _plan(hq, hkv, d, 0, n, dt, [1] * hkv)
+    plan, _ = _plan(hq, hkv, d, 0, n, dt, [1] * hkv)
     q, k, v = _inputs(bsz, n, hq, hkv, d, dtype, 7)
     o = M.moa_prefill(plan, q, k, v)
     torch.cuda.synchronize()
@@ -81,7 +85,7 @@ def test_prefill_window_one_no_sink_is_identity(dt):
 def test_prefill_full_window_equals_causal_attention():
     _say("prefill full window")
     bsz, n, h, d = 1, 600, 4, 128
-    plan = _plan(h, h, d, 0, n, "f32", [n] * h)
+    plan, _ = _plan(h, h, d, 0, n, "f32", [n] * h)
     q, k, v = _inputs(bsz, n, h, h, d, torch.float32, 9)
     o = M.moa_prefill(plan, q, k, v)
     tq, tk, tv = (x.double().cpu().permute(0, 2, 1, 3) for x in (q, k, v))
@@ -91,7 +95,7 @@ def test_prefill_full_window_equals_causal_attention():
 
 def test_prefill_is_deterministic():
     _say("prefill determinism")
-    plan = _plan(8, 2, 128, 16, 800, "bf16", [33, 400])
+    plan, _ = _plan(8, 2, 128, 16, 800, "bf16", [33, 400])
     q, k, v = _inputs(1, 800, 8, 2, 128, torch.bfloat16, 11)
     o1 = M.moa_prefill(plan, q, k, v)
     o2 = M.moa_prefill(plan, q, k, v)
@@ -115,14 +119,14 @@ def test_prefill_block_band_matches_oracle(case):
     dt, bsz, n, hq, hkv, d, s, windows = case
     _say("prefill block band", case)
     dtype = DT[dt]
-    plan = M.moa_plan(hq, hkv, d, s, n, dt, [float(w) for w in windows], [0.0] * hkv, flags=M.MOA_BLOCK_BAND)
-    assert list(plan.window) == [min(w, n) for w in windows]
+    plan, rw = _plan(hq, hkv, d, s, n, dt, windows, flags=M.MOA_BLOCK_BAND)
+    assert rw == [min(w, n) for w in windows]
     q, k, v = _inputs(bsz, n, hq, hkv, d, dtype, 200 + n)
     o, buf = guarded_empty(q.shape, dtype)
     M.moa_prefill(plan, q, k, v, o)
     torch.cuda.synchronize()
     assert guard_intact(buf, q.shape), "write past the output"
-    ref = oracle.attention_ref(q, k, v, plan.window, s, block=64)
+    ref = oracle.attention_ref(q, k, v, rw, s, block=64)
     assert_close(o, ref, dtype, with_rounding=True, what=f"block prefill {case}")
 
 
@@ -130,9 +134,8 @@ def test_span_includes_sinks_prefill_and_decode():
     _say("span includes sinks")
     alpha, beta, n, s = [100.0, 10.0, 5000.0, 300.5], [0.0, 0.0, 0.0, 0.1], 900, 64
     plan = M.moa_plan(8, 4, 128, s, n, "bf16", alpha, beta, flags=M.MOA_SPAN_INCLUDES_SINKS)
-    windows = oracle.plan_ref(alpha, beta, n, s, span_includes_sinks=True)["window"]
-    assert list(plan.window) == [36, 1, 836, 326]
-    assert np.array_equal(plan.window, windows)
+    windows = oracle_windows(plan, alpha, beta, span_includes_sinks=True)
+    assert windows == [36, 1, 836, 326]
     q, k, v = _inputs(2, n + 1, 8, 4, 128, torch.bfloat16, 77)
     o = M.moa_prefill(plan, q[:, :n].contiguous(), k[:, :n].contiguous(), v[:, :n].contiguous())
     kc, vc, pos = M.new_cache(plan, 2)
@@ -150,7 +153,8 @@ def test_span_includes_sinks_prefill_and_decode():
 def test_block_band_leaves_decode_token_exact():
     _say("block band decode")
     n, s, windows = 300, 4, [70, 129]
-    plan = M.moa_plan(4, 2, 128, s, n, "bf16", [float(w) for w in windows], [0.0, 0.0], flags=M.MOA_BLOCK_BAND)
+    plan, rw = _plan(4, 2, 128, s, n, "bf16", windows, flags=M.MOA_BLOCK_BAND)
+    assert rw == windows
     q, k, v = _inputs(1, n, 4, 2, 128, torch.bfloat16, 78)
     kc, vc, pos = M.new_cache(plan, 1)
     ws = M.new_workspace(plan, 1)
@@ -179,7 +183,7 @@ def test_kv_append_bulk_then_single_bit_exact(case):
     _say("append", case)
     dtype = DT[dt]
     total, n0 = 150, 90
-    plan = _plan(hkv, hkv, d, s, n0, dt, windows)
+    plan, rw = _plan(hkv, hkv, d, s, n0, dt, windows)
     k = workloads.randn((bsz, total, hkv, d), 21, dtype, "cuda")
     v = workloads.randn((bsz, total, hkv, d), 22, dtype, "cuda")
     kc, vc, pos = M.new_cache(plan, bsz)
@@ -188,7 +192,7 @@ def test_kv_append_bulk_then_single_bit_exact(case):
         M.moa_kv_append(plan, kc, vc, pos, k[:, t:t + 1].contiguous(), v[:, t:t + 1].contiguous(), t)
         if t in (n0, n0 + 1, total - 1):
             torch.cuda.synchronize()
-            epos, ek, ev = oracle.cache_contents_ref(k[:, : t + 1].cpu(), v[:, : t + 1].cpu(), plan.window, s)
+            epos, ek, ev = oracle.cache_contents_ref(k[:, : t + 1].cpu(), v[:, : t + 1].cpu(), rw, s)
             assert np.array_equal(pos.cpu().numpy(), epos), f"pos table after {t}"
             assert torch.equal(bits(kc), bits(ek)), f"K cache after {t}"
             assert torch.equal(bits(vc), bits(ev)), f"V cache after {t}"
@@ -197,7 +201,7 @@ def test_kv_append_bulk_then_single_bit_exact(case):
 def test_kv_append_chunked_equals_single():
     _say("append chunked")
     bsz, hkv, d, s = 2, 3, 128, 4
-    plan = _plan(hkv, hkv, d, s, 64, "bf16", [1, 13, 64])
+    plan, _ = _plan(hkv, hkv, d, s, 64, "bf16", [1, 13, 64])
     total = 200
     k = workloads.randn((bsz, total, hkv, d), 31, torch.bfloat16, "cuda")
     v = workloads.randn((bsz, total, hkv, d), 32, torch.bfloat16, "cuda")
@@ -220,7 +224,7 @@ def test_kv_append_chunked_equals_single():
 def _decode_run(dt, bsz, hq, hkv, d, s, windows, n0, steps, seed, poison=False):
     dtype = DT[dt]
     total = n0 + steps
-    plan = _plan(hq, hkv, d, s, max(n0, max(windows)), dt, windows)
+    plan, rw = _plan(hq, hkv, d, s, max(n0, max(windows)), dt, windows)
     q = workloads.randn((bsz, total, hq, d), seed, dtype, "cuda")
     k = workloads.randn((bsz, total, hkv, d), seed + 1, dtype, "cuda")
     v = workloads.randn((bsz, total, hkv, d), seed + 2, dtype, "cuda")
@@ -238,7 +242,7 @@ def _decode_run(dt, bsz, hq, hkv, d, s, windows, n0, steps, seed, poison=False):
     torch.cuda.synchronize()
     for t, o, buf in outs:
         assert guard_intact(buf, (bsz, hq, d)), f"write past decode output at {t}"
-        ref = oracle.decode_ref(q[:, t], k[:, : t + 1], v[:, : t + 1], plan.window, s)
+        ref = oracle.decode_ref(q[:, t], k[:, : t + 1], v[:, : t + 1], rw, s)
         assert_close(o, ref, dtype, with_rounding=True, what=f"decode t={t}")
     return plan, q, k, v
 
@@ -265,6 +269,14 @@ DECODE_CASES = [
     ("bf16", 4, 16, 2, 64, 3, [1, 2], 5, 4),                  # G = 8, one worker for the batch
     ("bf16", 8, 8, 8, 128, 64, [3000, 17, 900, 2999, 1, 1500, 333, 2000], 3000, 2),  # many workers
     ("bf16", 1, 16, 4, 64, 16, [30000, 5, 70000, 1], 70000, 2),  # G = 4, one cache over > 16 workers
+    # every other (dtype, head_dim, group) instantiation the plan accepts
+    ("bf16", 3, 4, 4, 64, 8, [10, 700, 1300, 64], 1400, 3),   # bf16 G = 1, head_dim 64
+    ("f32", 2, 4, 4, 128, 16, [1, 500, 1200, 77], 1300, 3),   # fp32 G = 1, head_dim 128
+    ("f32", 2, 8, 4, 64, 0, [1, 900, 64, 1500], 1600, 2),     # fp32 G = 2, head_dim 64
+    ("f32", 2, 8, 2, 64, 4, [300, 1900], 2000, 3),            # fp32 G = 4, head_dim 64
+    ("f32", 1, 16, 4, 128, 64, [5, 1025, 3000, 64], 3100, 2),  # fp32 G = 4, head_dim 128
+    ("f32", 2, 16, 2, 64, 3, [2500, 40], 2600, 2),            # fp32 G = 8, head_dim 64
+    ("f32", 1, 64, 8, 128, 64, [5000, 1, 3000, 64, 700, 4999, 128, 2048], 5100, 2),  # fp32 G = 8, head_dim 128
 ]
 
 
@@ -278,7 +290,7 @@ def test_decode_equals_prefill_row():
     _say("decode vs prefill row")
     bsz, hq, hkv, d, s, n = 2, 8, 2, 128, 8, 900
     windows = [50, 700]
-    plan = _plan(hq, hkv, d, s, n, "bf16", windows)
+    plan, _ = _plan(hq, hkv, d, s, n, "bf16", windows)
     q, k, v = _inputs(bsz, n, hq, hkv, d, torch.bfloat16, 60)
     o_pre = M.moa_prefill(plan, q, k, v)
     kc, vc, pos = M.new_cache(plan, bsz)
@@ -289,3 +301,44 @@ def test_decode_equals_prefill_row():
     torch.cuda.synchronize()
     diff = (o_dec.float() - o_pre[:, n - 1].float()).abs().max().item()
     assert diff <= BF16_ATOL, diff
+
+
+SPLIT_CASES = [
+    # dtype, Hq, Hkv, D, sinks, windows, context
+    ("bf16", 8, 8, 128, 16, [3000, 700, 1, 2999, 64, 1500, 2000, 10], 3000),   # vector-ALU kernel
+    ("bf16", 16, 4, 128, 64, [2500, 90, 1200, 2048], 2600),                     # matrix cores, G = 4
+    ("f32", 8, 2, 64, 4, [1900, 333], 2000),                                    # fp32, G = 4
+]
+
+
+@pytest.mark.parametrize("case", SPLIT_CASES, ids=lambda c: f"{c[0]}-hq{c[1]}-hkv{c[2]}-d{c[3]}")
+def test_decode_does_not_depend_on_the_work_split(case):
+    """A softmax over a set does not depend on how the set is partitioned
+    (Eq. 1).  The same sequence's caches are decoded inside a batch of 32 and
+    alone: the equal-work split over workers cuts its caches at different
+    keys (about 15 workers for the sequence alone, hundreds for the batch), so
+    the partial sums and their merge differ; the outputs must agree within the
+    floating-point bar, and both must match the oracle."""
+    dt, hq, hkv, d, s, windows, n = case
+    _say("split invariance", case)
+    dtype = DT[dt]
+    bsz = 32
+    plan, rw = _plan(hq, hkv, d, s, n, dt, windows)
+    q, k, v = _inputs(bsz, n + 1, hq, hkv, d, dtype, 90)
+    kc, vc, pos = M.new_cache(plan, bsz)
+    M.moa_kv_append(plan, kc, vc, pos, k[:, :n].contiguous(), v[:, :n].contiguous(), 0)
+    M.moa_kv_append(plan, kc, vc, pos, k[:, n:].contiguous(), v[:, n:].contiguous(), n)
+    ws = M.new_workspace(plan, bsz)
+    ws.fill_(0xFF)
+    o_batch = M.moa_decode(plan, q[:, n].contiguous(), kc, vc, n, ws)
+    ws1 = M.new_workspace(plan, 1)
+    ws1.fill_(0xFF)
+    tol = F32_ATOL if dtype == torch.float32 else BF16_ATOL
+    for j in (0, 13, 31):
+        o_one = M.moa_decode(plan, q[j:j + 1, n].contiguous(), kc[j:j + 1].clone(), vc[j:j + 1].clone(), n, ws1)
+        torch.cuda.synchronize()
+        diff = (o_one.double() - o_batch[j:j + 1].double()).abs().max().item()
+        assert diff <= tol, f"sequence {j}: batch-of-32 vs alone differ by {diff}"
+        ref = oracle.decode_ref(q[j:j + 1, n], k[j:j + 1], v[j:j + 1], rw, s)
+        assert_close(o_one, ref, dtype, with_rounding=True, what=f"alone j={j}")
+        assert_close(o_batch[j:j + 1], ref, dtype, with_rounding=True, what=f"in batch j={j}")

@@ -5,7 +5,7 @@ import torch
 
 import oracle
 import workloads
-from helpers import assert_close, bits
+from helpers import assert_close, bits, oracle_windows
 from paper_2406_14909_amd import moa as M
 
 pytestmark = pytest.mark.gpu
@@ -25,6 +25,7 @@ def test_ragged_append_and_decode(dt, hq, hkv, d, s, windows, lengths):
     bsz, steps = len(lengths), 3
     plan = M.moa_plan(hq, hkv, d, s, max(max(windows), max(lengths)), dt, [float(w) for w in windows],
                       [0.0] * hkv)
+    rw = oracle_windows(plan, windows, [0.0] * hkv)
     total = max(lengths) + steps
     q = workloads.randn((bsz, total, hq, d), 70, dtype, "cuda")
     k = workloads.randn((bsz, total, hkv, d), 71, dtype, "cuda")
@@ -53,7 +54,7 @@ def test_ragged_append_and_decode(dt, hq, hkv, d, s, windows, lengths):
                 assert torch.all(o[b] == 7.0), "inactive sequence was written"
                 continue
             t = cur[b]
-            ref = oracle.decode_ref(q[b:b + 1, t], k[b:b + 1, : t + 1], v[b:b + 1, : t + 1], plan.window, s)
+            ref = oracle.decode_ref(q[b:b + 1, t], k[b:b + 1, : t + 1], v[b:b + 1, : t + 1], rw, s)
             assert_close(o[b:b + 1], ref, dtype, with_rounding=True, what=f"ragged b={b} t={t}")
         for b in range(bsz):
             if b != inactive:
@@ -61,7 +62,7 @@ def test_ragged_append_and_decode(dt, hq, hkv, d, s, windows, lengths):
     for b in range(bsz):
         n_done = cur[b]
         epos, ek, ev = oracle.cache_contents_ref(k[b:b + 1, :n_done].cpu(), v[b:b + 1, :n_done].cpu(),
-                                                 plan.window, s)
+                                                 rw, s)
         assert np.array_equal(pos[b:b + 1].cpu().numpy(), epos), f"pos table of sequence {b}"
         assert torch.equal(bits(kc[b:b + 1]), bits(ek)) and torch.equal(bits(vc[b:b + 1]), bits(ev))
 
@@ -96,6 +97,7 @@ def test_long_context_batch1_decode_sampled():
     _say("decode", wl.name)
     n, steps = wl.n, 2
     plan = M.moa_plan(wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.num_sink, n, wl.dtype, wl.alpha, wl.beta)
+    rw = oracle_windows(plan, wl.alpha, wl.beta)
     k = workloads.randn((1, n + steps, wl.num_kv_heads, wl.head_dim), 90, torch.bfloat16, "cuda")
     v = workloads.randn((1, n + steps, wl.num_kv_heads, wl.head_dim), 91, torch.bfloat16, "cuda")
     q = workloads.randn((steps, 1, wl.num_q_heads, wl.head_dim), 92, torch.bfloat16, "cuda")
@@ -113,5 +115,5 @@ def test_long_context_batch1_decode_sampled():
         for i in range(steps):
             t = n + i
             ref = oracle.decode_ref(q[i, :, g:g + 1].cpu(), kb[:, : t + 1], vb[:, : t + 1],
-                                    [int(plan.window[g])], wl.num_sink)
+                                    [rw[g]], wl.num_sink)
             assert_close(outs[i][:, g:g + 1], ref, torch.bfloat16, what=f"128k t={t} h={g}")

@@ -101,11 +101,12 @@ def test_profile_loss_select_plan_loop():
     assert loss == pytest.approx(ref_loss, abs=tol)
     # the chosen rules make a working plan
     plan = M.moa_plan(h, h, d, s, n, "bf16", a[rules], b[rules], flags=flags)
-    assert np.array_equal(plan.window, oracle.plan_ref(a[rules], b[rules], n, s, span_includes_sinks=True)["window"])
+    rw = oracle.plan_ref(a[rules], b[rules], n, s, span_includes_sinks=True)["window"]
+    assert np.array_equal(plan.window, rw)
     kc, vc, pos = M.new_cache(plan, bsz)
     ws = M.new_workspace(plan, bsz)
     M.moa_kv_append(plan, kc, vc, pos, k, v, 0)
     od = M.moa_decode(plan, q[:, n - 1].contiguous(), kc, vc, n - 1, ws)
     torch.cuda.synchronize()
-    ref = oracle.decode_ref(q[:, n - 1], k, v, plan.window, s)
+    ref = oracle.decode_ref(q[:, n - 1], k, v, rw, s)
     assert np.abs(od.float().cpu().numpy() - ref).max() <= 1e-2
