@@ -194,6 +194,24 @@ moa_status_t moa_decode(const moa_plan_t* plan, const void* q, const void* k_cac
                         const void* v_cache, void* o, int32_t batch, int64_t pos,
                         void* workspace, size_t ws_bytes, void* hip_stream);
 
+/* Decode for callers that cannot allocate device memory or pass a workspace
+ * (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): moa_decode with the split-K partials kept in a workspace that
+ * the library owns, a fixed array of MOA_DECODE_SCRATCH_BYTES per GPU
+ * (allocated when the library's code is loaded on that device and held until
+ * the process ends).  Same arguments, layouts and result as moa_decode, minus
+ * the workspace; the call allocates nothing (no hipMalloc, no library that
+ * allocates).  Returns MOA_ERR_WORKSPACE, launching nothing, when
+ * moa_decode_workspace_bytes(plan, batch) exceeds MOA_DECODE_SCRATCH_BYTES
+ * (e.g. head_dim 128 with group 8 allows batch * num_kv_heads <= 7695).
+ * Every call on one GPU shares that GPU's array: calls that overlap in time
+ * on one GPU (other streams, other host threads) race and give wrong
+ * results, so order them on one stream.  The array needs no clearing: each
+ * partial is written before it is read within the same call. */
+#define MOA_DECODE_SCRATCH_BYTES (64u << 20)
+moa_status_t moa_decode_noalloc(const moa_plan_t* plan, const void* q, const void* k_cache,
+                                const void* v_cache, void* o, int32_t batch, int64_t pos, void* hip_stream);
+
 /* One-token append at per-sequence positions (paper Appendix "Efficiency
  * Experiment Setup": the newest token replaces the oldest entry beyond the
  * span; each sequence of a serving batch may be at its own position).

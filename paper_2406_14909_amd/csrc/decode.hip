@@ -37,10 +37,38 @@
 //                  step is permuted identically on both operands.
 #include <algorithm>
 #include <atomic>
+#include <mutex>
 
 #include "moa_device.h"
 
 namespace moa {
+
+// Library-owned decode workspace for callers that cannot allocate
+// (moa_decode_noalloc): kDecodeScratchBytes of fp32 split-K partials, one copy
+// per GPU the library runs on, held until the process ends.  Host code never
+// passes the array's name to a kernel (on the host it is only a stand-in for
+// the symbol): decode_scratch() resolves each device's own address once with
+// hipGetSymbolAddress and kernels get that address.
+__device__ __align__(256) float scratch[kDecodeScratchBytes / sizeof(float)];
+
+int decode_scratch(void** out) {
+  static std::mutex mu;
+  static void* addr[64] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return static_cast<int>(e);
+  if (dev < 0 || dev >= 64) return static_cast<int>(hipErrorInvalidDevice);
+  std::lock_guard<std::mutex> lock(mu);
+  if (addr[dev] == nullptr) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return static_cast<int>(e);
+    if (p == nullptr) return static_cast<int>(hipErrorInvalidSymbol);
+    addr[dev] = p;
+  }
+  *out = addr[dev];
+  return 0;
+}
 
 namespace {
 

@@ -335,6 +335,38 @@ moa_status_t moa_decode(const moa_plan_t* plan, const void* q, const void* k_cac
   return ok();
 }
 
+moa_status_t moa_decode_noalloc(const moa_plan_t* plan, const void* q, const void* k_cache,
+                                const void* v_cache, void* o, int32_t batch, int64_t pos, void* hip_stream) {
+  if (!plan) return fail(MOA_ERR_INVALID_ARG, "moa_decode_noalloc: null plan");
+  if (!q || !k_cache || !v_cache || !o) return fail(MOA_ERR_INVALID_ARG, "moa_decode_noalloc: null tensor pointer");
+  if (batch < 1) return fail(MOA_ERR_INVALID_ARG, "moa_decode_noalloc: batch must be >= 1");
+  if (pos < 0 || pos >= (int64_t(1) << 31) - 1)
+    return fail(MOA_ERR_INVALID_ARG, "moa_decode_noalloc: pos must be in [0, 2^31 - 1)");
+  if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(o))
+    return fail(MOA_ERR_INVALID_ARG, "moa_decode_noalloc: tensors must be 16-byte aligned");
+  const size_t need = decode_workspace_bytes(*plan, batch);
+  if (need > kDecodeScratchBytes)
+    return fail(MOA_ERR_WORKSPACE, "moa_decode_noalloc: this plan and batch need " + std::to_string(need) +
+                                       " bytes of decode workspace, more than the library's " +
+                                       std::to_string(kDecodeScratchBytes) + " (MOA_DECODE_SCRATCH_BYTES); "
+                                       "use moa_decode with a caller-owned workspace");
+  void* ws = nullptr;
+  const int serr = decode_scratch(&ws);
+  if (serr) return fail(MOA_ERR_HIP, "moa_decode_noalloc: hipGetSymbolAddress of the decode workspace failed (hipError " +
+                                         std::to_string(serr) + ")");
+  if (decode_overlap(*plan, q, k_cache, v_cache, o, batch, ws, need))
+    return fail(MOA_ERR_INVALID_ARG, "moa_decode_noalloc: o overlaps another argument");
+  const moa_desc_t& d = plan->desc;
+  int64_t seg_len[MOA_MAX_KV_HEADS];
+  for (int h = 0; h < d.num_kv_heads; ++h) seg_len[h] = std::min<int64_t>(pos + 1, plan->capacity[h]);
+  DecodeArgs a;
+  const moa_status_t st = decode_args(*plan, "moa_decode_noalloc", q, k_cache, v_cache, o, batch, ws, seg_len, &a);
+  if (st != MOA_OK) return st;
+  const int err = launch_decode(a, d.dtype, d.head_dim, plan->group, hip_stream);
+  if (err) return fail(MOA_ERR_HIP, "moa_decode_noalloc: kernel launch failed (hipError " + std::to_string(err) + ")");
+  return ok();
+}
+
 moa_status_t moa_decode_ragged(const moa_plan_t* plan, const void* q, const void* k_cache,
                                const void* v_cache, void* o, const int32_t* positions, int32_t batch,
                                void* workspace, size_t ws_bytes, void* hip_stream) {

@@ -137,6 +137,9 @@ int launch_kv_append(const AppendArgs& a, int dtype, int head_dim, void* stream)
 int launch_decode(DecodeArgs a, int dtype, int head_dim, int group, void* stream);
 int launch_influence(const InfluenceArgs& a, int head_dim, void* stream);
 int launch_rule_loss(const RuleLossArgs& a, void* stream);
+// Device address of the library-owned decode workspace on the current device
+// (resolved once per device); returns a hipError_t as int.
+int decode_scratch(void** out);
 
 constexpr int kPrefillRows = 128;   // query rows per prefill work-group
 constexpr int kPrefillChunk = 16;   // minimum query tiles per prefill dispatch unit
@@ -145,6 +148,7 @@ constexpr int kNumXcd = 8;          // accelerator dies; work-groups go round-ro
 constexpr int kMaxDecodeWorkers = 8192;  // decode workers (waves) per launch, at most
 constexpr int kDecodeMinKeys = 256;      // virtual keys per decode worker, at least
 constexpr int kDecodePartPad = 4;        // partial row: head_dim sums, m, l, 2 pad floats
+constexpr size_t kDecodeScratchBytes = MOA_DECODE_SCRATCH_BYTES;   // library-owned decode workspace per GPU
 constexpr int kInfluenceBlock = 64;      // profiling block (tokens)
 constexpr int kMaxInfluenceN = 65536;    // longest profiled sequence (block sums stay in LDS)
 

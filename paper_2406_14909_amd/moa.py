@@ -24,7 +24,7 @@ MOA_MAX_Q_HEADS = 512
 EXPORTED = (
     "moa_plan", "moa_plan_tables", "moa_plan_free", "moa_prefill", "moa_kv_append",
     "moa_decode_workspace_bytes", "moa_decode", "moa_last_error", "moa_kv_append_ragged",
-    "moa_decode_ragged", "moa_influence", "moa_rule_loss",
+    "moa_decode_ragged", "moa_influence", "moa_rule_loss", "moa_decode_noalloc",
 )
 
 
@@ -86,6 +86,8 @@ def load_library(path: Optional[str] = None) -> ctypes.CDLL:
     lib.moa_decode.restype = ctypes.c_int
     lib.moa_kv_append_ragged.argtypes = [vp, vp, vp, vp, vp, vp, vp, i32, vp]
     lib.moa_kv_append_ragged.restype = ctypes.c_int
+    lib.moa_decode_noalloc.argtypes = [vp, vp, vp, vp, vp, i32, i64, vp]
+    lib.moa_decode_noalloc.restype = ctypes.c_int
     lib.moa_decode_ragged.argtypes = [vp, vp, vp, vp, vp, vp, i32, vp, ctypes.c_size_t, vp]
     lib.moa_decode_ragged.restype = ctypes.c_int
     lib.moa_influence.argtypes = [ctypes.POINTER(moa_desc_t), vp, vp, vp, vp, vp, i32, i64, vp]
@@ -275,6 +277,28 @@ def moa_decode(plan: Plan, q, k_cache, v_cache, pos: int, workspace, o=None, str
         _check(load_library().moa_decode(plan.handle, q.data_ptr(), k_cache.data_ptr(),
                                          v_cache.data_ptr(), o.data_ptr(), bsz, int(pos),
                                          workspace.data_ptr(), nbytes, _stream(q, stream)))
+    return o
+
+
+MOA_DECODE_SCRATCH_BYTES = 64 << 20
+
+
+def moa_decode_noalloc(plan: Plan, q, k_cache, v_cache, pos: int, o, stream=None):
+    """moa_decode without a caller workspace: the library keeps the split-K
+    partials in its own fixed per-GPU array (MOA_DECODE_SCRATCH_BYTES), so the
+    call allocates nothing; o must be given (q, o: [B, H_q, D]).  Calls that
+    overlap in time on one GPU share that array and race."""
+    bsz = int(q.shape[0])
+    dt = plan.torch_dtype
+    _need(q, (bsz, plan.num_q_heads, plan.head_dim), dt, "q")
+    _need(k_cache, (bsz, plan.cache_rows, plan.head_dim), dt, "k_cache")
+    _need(v_cache, (bsz, plan.cache_rows, plan.head_dim), dt, "v_cache")
+    _need(o, q.shape, dt, "o")
+    import torch
+    with torch.cuda.device(_one_device(q=q, k_cache=k_cache, v_cache=v_cache, o=o)):
+        _check(load_library().moa_decode_noalloc(plan.handle, q.data_ptr(), k_cache.data_ptr(),
+                                                 v_cache.data_ptr(), o.data_ptr(), bsz, int(pos),
+                                                 _stream(q, stream)))
     return o
 
 

@@ -186,6 +186,27 @@ def test_gpu_entry_points_validate_before_launch():
         assert st == M.MOA_ERR_INVALID_ARG and "overlap" in lib.moa_last_error().decode(), args
 
 
+def test_noalloc_decode_validates_before_launch():
+    # Invalid calls return before any HIP call; a plan and batch whose partials
+    # exceed the library's own array are refused with MOA_ERR_WORKSPACE.
+    p = _plan([100.0, 200.0], [0.0, 0.0], 1024, 4, hq=4, hkv=2)
+    h = p.handle
+    fake = 1 << 20
+    assert lib.moa_decode_noalloc(None, fake, fake, fake, fake, 2, 0, None) == M.MOA_ERR_INVALID_ARG
+    assert lib.moa_decode_noalloc(h, None, fake, fake, fake, 2, 0, None) == M.MOA_ERR_INVALID_ARG
+    assert lib.moa_decode_noalloc(h, fake, fake, fake, fake, 0, 0, None) == M.MOA_ERR_INVALID_ARG
+    assert lib.moa_decode_noalloc(h, fake, fake, fake, fake, 2, -1, None) == M.MOA_ERR_INVALID_ARG
+    assert lib.moa_decode_noalloc(h, fake + 8, fake, fake, fake, 2, 0, None) == M.MOA_ERR_INVALID_ARG
+    g8 = _plan([1.0] * 8, [0.0] * 8, 4, 0, hq=64, hkv=8)
+    assert M.moa_decode_workspace_bytes(g8, 961) <= M.MOA_DECODE_SCRATCH_BYTES    # 961 * 8 = 7688
+    assert M.moa_decode_workspace_bytes(g8, 962) > M.MOA_DECODE_SCRATCH_BYTES   # 962 * 8 = 7696
+    st = lib.moa_decode_noalloc(g8.handle, fake, 2 * fake, 3 * fake, 4 * fake, 962, 0, None)
+    assert st == M.MOA_ERR_WORKSPACE and "moa_decode with a caller-owned workspace" in lib.moa_last_error().decode()
+    text = open(os.path.join(ROOT, "include", "moa.h")).read()
+    assert int(re.search(r"#define MOA_DECODE_SCRATCH_BYTES \((\d+)u << (\d+)\)", text).group(1)) << 20 == \
+        M.MOA_DECODE_SCRATCH_BYTES
+
+
 def test_decode_workspace_size():
     # Partials for at most 8192 workers plus one per (sequence, KV head), each
     # group x (head_dim + 4) floats; independent of the cache lengths.
