@@ -196,6 +196,10 @@ def main() -> int:
     ap.add_argument("--span-includes-sinks", action="store_true",
                     help="the elastic rule gives the whole span, sinks included")
     ap.add_argument("--cpu-budget", type=float, default=12.0, help="seconds per oracle leg")
+    ap.add_argument("--no-configs", action="store_true",
+                    help="skip the per-configuration prefill / decode measurements of the other workloads")
+    ap.add_argument("--configs-reps", type=int, default=32,
+                    help="timed decode calls per configuration (prefill: a quarter of it, at least 5)")
     ap.add_argument("--profile-kernel", choices=["decode", "prefill", "append", "copy"], default=None,
                     help="launch only this kernel --reps times on the bench workload (hardware-counter runs)")
     ap.add_argument("--reps", type=int, default=3)
@@ -361,7 +365,7 @@ def main() -> int:
             "batch": B, "context": N, "decode_steps": steps_dec,
             "num_q_heads": Hq, "num_kv_heads": Hkv, "head_dim": D, "num_sink": s,
             "mean_window": float(np.mean(windows)),
-            "density": float(np.mean(caps)) / N,
+            "density": float(np.mean([min(c, N) for c in caps])) / N,
             "parallelism": "single GPU",
             "cache_sets": R,
             "plan_flags": [name for name, on in (("block_band", args.block_band),
@@ -398,11 +402,129 @@ def main() -> int:
         },
     }
 
+    if not args.no_configs:
+        result["configs"] = measure_configs(M, workloads, args.configs_reps)
     if not args.no_cpu_baseline:
         result["cpu_baseline"] = cpu_baseline(wl, plan, block, q_pre, k_pre, v_pre, q_dec, k_dec, v_dec,
                                               steps_dec, args.cpu_budget)
     print(json.dumps(result), flush=True)
     return 0
+
+
+class CallTimer:
+    """Times individual launches on torch's current stream with fence-free
+    event pairs; median milliseconds per call."""
+
+    def __init__(self, calls: int):
+        import torch
+
+        self.stream = torch.cuda.current_stream()
+        self.ev = TimingEvents(calls)
+        self.n = 0
+
+    def __call__(self, fn):
+        i = self.n
+        self.ev.record(i, 0, self.stream)
+        fn()
+        self.ev.record(i, 1, self.stream)
+        self.n += 1
+
+    def median_ms(self) -> float:
+        import torch
+
+        torch.cuda.synchronize()
+        ms = sorted(self.ev.ms(i) for i in range(self.n))
+        self.ev.close()
+        return float(ms[len(ms) // 2])
+
+
+def measure_configs(M, workloads, reps: int):
+    """Prefill and decode of the other workload shapes, each in the launch
+    configuration the paper's efficiency setup describes (one layer; decode
+    after a full-context prefill, appending one token per step).
+
+    prefill: moa_prefill of the workload's prefill batch at N tokens, median
+      of max(5, reps // 4) calls after 3 warm-ups; in-band TFLOP/s = 4 * D *
+      visible pairs / time (masked entries of executed tiles not counted).
+    decode: moa_decode at the workload's decode batch over 4 independent
+      cache sets decoded in rotation (each call reads data the 256 MB
+      last-level cache does not hold: the sets are 0.27-0.54 GB each), one
+      append per call, positions advancing; median of `reps` calls after 8
+      warm-ups; GB/s = filled-slot K/V bytes + q + o per call / time."""
+    import torch
+
+    out = {}
+    for name, do_prefill, do_decode in (("vicuna7b-prefill-n4096", True, False),
+                                        ("llama3-8b-gqa-n16384", True, True),
+                                        ("llama3-70b-gqa-n32768", True, True)):
+        wl = workloads.workload(name)
+        N, Hq, Hkv, D, s = wl.n, wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.num_sink
+        esz = 2
+        group = Hq // Hkv
+        plan = M.moa_plan(Hq, Hkv, D, s, N, wl.dtype, wl.alpha, wl.beta)
+        windows = [int(x) for x in plan.window]
+        caps = [int(x) for x in plan.capacity]
+        entry = {"num_q_heads": Hq, "num_kv_heads": Hkv, "head_dim": D, "num_sink": s, "context": N,
+                 "mean_window": float(np.mean(windows)), "density": float(np.mean([min(c, N) for c in caps])) / N}
+        log(f"[bench] config {name}")
+        if do_prefill:
+            B = wl.prefill_batch
+            q = workloads.randn((B, N, Hq, D), wl.seed * 10 + 7, torch.bfloat16, "cuda")
+            k = workloads.randn((B, N, Hkv, D), wl.seed * 10 + 8, torch.bfloat16, "cuda")
+            v = workloads.randn((B, N, Hkv, D), wl.seed * 10 + 9, torch.bfloat16, "cuda")
+            o = torch.empty_like(q)
+            for _ in range(3):
+                M.moa_prefill(plan, q, k, v, o)
+            n_calls = max(5, reps // 4)
+            timer = CallTimer(n_calls)
+            for _ in range(n_calls):
+                timer(lambda: M.moa_prefill(plan, q, k, v, o))
+            ms = timer.median_ms()
+            flops = 4.0 * D * B * group * sum(visible_pairs(N, w, s) for w in windows)
+            tf = flops / (ms / 1e3) / 1e12
+            entry["prefill"] = {"batch": B, "ms": round(ms, 4), "inband_tflops": round(tf, 2),
+                                "peak": BF16_MFMA_PEAK_TFLOPS, "frac": round(tf / BF16_MFMA_PEAK_TFLOPS, 4),
+                                "flops_per_launch": flops, "kernel": f"prefill_kernel<bf16,{D}>",
+                                "calls_timed": n_calls}
+            del q, k, v, o
+        if do_decode:
+            B, sets_n = wl.decode_batch, 4
+            k = workloads.randn((B, N, Hkv, D), wl.seed * 10 + 5, torch.bfloat16, "cuda")
+            v = workloads.randn((B, N, Hkv, D), wl.seed * 10 + 6, torch.bfloat16, "cuda")
+            total_calls = 8 + reps
+            steps = -(-total_calls // sets_n)
+            kn = workloads.randn((steps, B, 1, Hkv, D), wl.seed * 10 + 10, torch.bfloat16, "cuda")
+            vn = workloads.randn((steps, B, 1, Hkv, D), wl.seed * 10 + 11, torch.bfloat16, "cuda")
+            qn = workloads.randn((sets_n, B, Hq, D), wl.seed * 10 + 12, torch.bfloat16, "cuda")
+            sets = [M.new_cache(plan, B) for _ in range(sets_n)]
+            for c in sets:
+                M.moa_kv_append(plan, *c, k, v, 0)
+            del k, v
+            ws = M.new_workspace(plan, B)
+            o = torch.empty((B, Hq, D), dtype=torch.bfloat16, device="cuda")
+            timer = CallTimer(reps)
+            nbytes = []
+            for i in range(total_calls):
+                r, t = i % sets_n, N + i // sets_n
+                M.moa_kv_append(plan, *sets[r], kn[i // sets_n], vn[i // sets_n], t)
+                call = (lambda r=r, t=t: M.moa_decode(plan, qn[r], sets[r][0], sets[r][1], t, ws, o))
+                if i < 8:
+                    call()
+                else:
+                    timer(call)
+                    nbytes.append(B * sum(min(t + 1, c) for c in caps) * D * 2 * esz + 2 * B * Hq * D * esz)
+            ms = timer.median_ms()
+            gbs = float(np.mean(nbytes)) / (ms / 1e3) / 1e9
+            kern = f"decode_mma_kernel<{D},{group}>" if group >= 2 else f"decode_valu_kernel<bf16,{D},1>"
+            entry["decode"] = {"batch": B, "us_per_call": round(ms * 1e3, 2), "hbm_gbs": round(gbs, 1),
+                               "peak": HBM_PEAK_GBS, "frac": round(gbs / HBM_PEAK_GBS, 4),
+                               "tokens_per_s": round(B / (ms / 1e3), 1),
+                               "bytes_per_call": round(float(np.mean(nbytes))), "cache_sets": sets_n,
+                               "kernel": f"moa_decode ({kern} + decode_combine_kernel)", "calls_timed": reps}
+            del sets, kn, vn, qn, ws, o
+        torch.cuda.empty_cache()
+        out[name] = entry
+    return out
 
 
 def measure_influence(args):
@@ -584,13 +706,26 @@ def profile_kernel(args, M, plan, q_pre, k_pre, v_pre, o_pre, q_dec, k_dec, v_de
     return 0
 
 
+def cpu_model() -> str:
+    """The host CPU's model name (from /proc/cpuinfo), or "unknown"."""
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.lower().startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(wl, plan, block, q_pre, k_pre, v_pre, q_dec, k_dec, v_dec, steps_dec, budget):
     """Times the fp64 oracle on a bounded sample of the same step and scales it.
 
-    Sample: prefill rows of sequence 0 (all query heads, rows spread over the
-    sequence) and decode tokens of sequence 0 (all heads, the first decode
-    position), each leg run for about `budget` seconds.  The whole-step time is
-    extrapolated by row count: B*N prefill rows + B*steps decode tokens.
+    Prefill leg: the oracle's row-blocked dense-masked attention (blocks of
+    1024 rows x all keys, BLAS products) over whole query heads of sequence 0,
+    one head at a time, for about `budget` seconds.  Decode leg: decode tokens
+    of sequence 0 (all heads, the first decode position) for about `budget`
+    seconds.  The whole-step time is extrapolated by count: B * H_q prefill
+    heads + B * steps decode tokens.
     """
     import numpy as np
     import torch
@@ -603,18 +738,17 @@ def cpu_baseline(wl, plan, block, q_pre, k_pre, v_pre, q_dec, k_dec, v_dec, step
         cores = os.cpu_count() or 1
 
     B, N, Hq = wl.decode_batch, wl.n, wl.num_q_heads
+    group = Hq // wl.num_kv_heads
     log("[bench] timing the CPU oracle on a bounded sample")
-    # prefill rows of sequence 0
     qc, kc, vc = (x[0:1].cpu() for x in (q_pre, k_pre, v_pre))
-    rng = np.random.default_rng(0)
-    rows_done, t0 = 0, time.perf_counter()
-    while time.perf_counter() - t0 < budget:
-        rows = np.sort(rng.integers(0, N, 8))
-        for h in range(Hq):
-            oracle.attention_rows_ref(qc, kc, vc, plan.window, wl.num_sink, 0, h, rows, block=block)
-        rows_done += len(rows)
-    t_row = (time.perf_counter() - t0) / rows_done          # one row, all heads
-    # decode tokens of sequence 0 at the first decode position
+    heads_done, t0 = 0, time.perf_counter()
+    while time.perf_counter() - t0 < budget or heads_done == 0:
+        h = heads_done % Hq
+        g = h // group
+        oracle.attention_ref(qc[:, :, h:h + 1], kc[:, :, g:g + 1], vc[:, :, g:g + 1], [int(plan.window[g])],
+                             wl.num_sink, block=block)
+        heads_done += 1
+    t_head = (time.perf_counter() - t0) / heads_done          # one head, all N rows
     t = N
     k_hist = torch.cat([kc, k_dec[0, 0:1].cpu()], dim=1)
     v_hist = torch.cat([vc, v_dec[0, 0:1].cpu()], dim=1)
@@ -624,16 +758,18 @@ def cpu_baseline(wl, plan, block, q_pre, k_pre, v_pre, q_dec, k_dec, v_dec, step
         oracle.decode_ref(qt, k_hist, v_hist, plan.window, wl.num_sink)
         dec_done += 1
     t_tok = (time.perf_counter() - t0) / dec_done            # one token, all heads
-    step_s = B * N * t_row + B * steps_dec * t_tok
+    step_s = B * Hq * t_head + B * steps_dec * t_tok
     return {
         "value": round(B * steps_dec / step_s, 4),
         "unit": "tokens/s",
         "cores": int(cores),
+        "cpu_model": cpu_model(),
         "kind": "oracle",
-        "sample": (f"fp64 oracle on sequence 0: {rows_done} prefill rows x {Hq} heads and "
-                   f"{dec_done} decode tokens x {Hq} heads at context {t}; extrapolated by row "
-                   f"count to the whole step ({B}x{N} prefill rows + {B}x{steps_dec} decode tokens)"),
-        "seconds_per_prefill_row": t_row,
+        "sample": (f"fp64 oracle on sequence 0: {heads_done} whole prefill heads ({N} rows each, row-blocked "
+                   f"1024 x {N} BLAS products) and {dec_done} decode tokens x {Hq} heads at context {t}; "
+                   f"extrapolated by count to the whole step ({B}x{Hq} prefill heads + {B}x{steps_dec} "
+                   f"decode tokens)"),
+        "seconds_per_prefill_head": t_head,
         "seconds_per_decode_token": t_tok,
         "extrapolated_step_s": step_s,
     }

@@ -15,8 +15,8 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 def test_bench_line_carries_the_contract():
     print("[case] bench.py small-mha4-d64-n512-f32", flush=True)
     cmd = [sys.executable, os.path.join(ROOT, "bench.py"), "--workload", "small-mha4-d64-n512-f32",
-           "--steps", "2", "--warmup", "1", "--cpu-budget", "0.5"]
-    r = subprocess.run(cmd, cwd=ROOT, stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True, timeout=110)
+           "--steps", "2", "--warmup", "1", "--cpu-budget", "0.5", "--configs-reps", "8"]
+    r = subprocess.run(cmd, cwd=ROOT, stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True, timeout=240)
     assert r.returncode == 0, r.stderr[-2000:]
     lines = [l for l in r.stdout.splitlines() if l.startswith("{")]
     assert len(lines) == 1, r.stdout
@@ -34,3 +34,14 @@ def test_bench_line_carries_the_contract():
     assert "traffic" in roof
     cpu = d["cpu_baseline"]
     assert cpu["kind"] == "oracle" and cpu["value"] > 0 and cpu["cores"] >= 1 and cpu["sample"]
+    assert cpu["cpu_model"]
+    # the other workload shapes: prefill of three, decode of the two GQA layers
+    cfg = d["configs"]
+    assert set(cfg) == {"vicuna7b-prefill-n4096", "llama3-8b-gqa-n16384", "llama3-70b-gqa-n32768"}
+    for name, entry in cfg.items():
+        pre = entry["prefill"]
+        assert pre["inband_tflops"] > 0 and abs(pre["frac"] - pre["inband_tflops"] / pre["peak"]) < 1e-3
+        if name != "vicuna7b-prefill-n4096":
+            dec = entry["decode"]
+            assert dec["cache_sets"] >= 4 and dec["hbm_gbs"] > 0
+            assert abs(dec["frac"] - dec["hbm_gbs"] / dec["peak"]) < 1e-3
