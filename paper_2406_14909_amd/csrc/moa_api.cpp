@@ -216,6 +216,9 @@ moa_status_t moa_prefill(const moa_plan_t* plan, const void* q, const void* k, c
   a.scale_log2 = plan->scale * 1.4426950408889634f;
   a.band_shift = (d.flags & MOA_BLOCK_BAND) ? 6 : 0;
   static_assert(MOA_BAND_BLOCK == 64, "band_shift is log2(MOA_BAND_BLOCK)");
+  // Keys and values larger than the last-level cache are re-read from HBM by
+  // the band sweeps of different query tiles unless those sweeps run in step.
+  a.rotate = 2 * static_cast<int64_t>(kbytes) > kLastLevelCacheBytes ? 1 : 0;
   for (int h = 0; h < d.num_kv_heads; ++h) {
     // Band length in tokens, or in blocks of MOA_BAND_BLOCK tokens (rounded up).
     a.window[h] = (d.flags & MOA_BLOCK_BAND) ? (plan->window[h] + MOA_BAND_BLOCK - 1) / MOA_BAND_BLOCK

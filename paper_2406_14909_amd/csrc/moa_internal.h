@@ -47,6 +47,7 @@ struct PrefillArgs {
   int32_t n_units;           // hkv * batch * n_chunks
   float scale_log2;          // softmax scale * log2(e)
   int32_t band_shift;        // the band of row i starts at ((i >> shift) - window + 1) << shift
+  int32_t rotate;            // visit each unit's band tiles in step (keys and values exceed the last-level cache)
   int32_t window[MOA_MAX_KV_HEADS];   // band length in units of 2^band_shift tokens
   int16_t kv_order[MOA_MAX_KV_HEADS];
 };
@@ -145,6 +146,7 @@ constexpr int kPrefillRows = 128;   // query rows per prefill work-group
 constexpr int kPrefillChunk = 16;   // minimum query tiles per prefill dispatch unit
 constexpr int kPrefillUnitBlocks = 64;  // minimum work-groups per prefill dispatch unit
 constexpr int kNumXcd = 8;          // accelerator dies; work-groups go round-robin over them
+constexpr int64_t kLastLevelCacheBytes = int64_t(256) << 20;   // MI355X Infinity Cache
 constexpr int kMaxDecodeWorkers = 8192;  // decode workers (waves) per launch, at most
 constexpr int kDecodeMinKeys = 256;      // virtual keys per decode worker, at least
 constexpr int kDecodePartPad = 4;        // partial row: head_dim sums, m, l, 2 pad floats

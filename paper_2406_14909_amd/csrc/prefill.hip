@@ -217,7 +217,25 @@ __global__ void __launch_bounds__(NW * 64, 2) prefill_kernel(PrefillArgs a) {
     k_src[i] = uint32_t(r) * uint32_t(kv_row_bytes) + uint32_t(p ^ TL::swz_k(r)) * 16u;
     if constexpr (TL::kTr) v_src[i] = uint32_t(r) * uint32_t(kv_row_bytes) + uint32_t(p ^ TL::swz_v(r)) * 16u;
   }
-  auto tile_j0 = [&](int it) { return (it < ta ? it : tb + (it - ta)) * BN; };
+  // With a.rotate the band tiles are visited in a rotated order: from the
+  // unit's common start tile tr (the first band tile of its last query tile,
+  // clipped to this work-group's band) up to tl, then from tb up to tr - 1.
+  // The work-groups of a unit run side by side on one die, so at every step
+  // they read the same key tile (before the wrap: tile tr + step; after it:
+  // tile tb + step - (tl - tr + 1), the same for every work-group since tb
+  // and tl move with the query tile in step), and each tile comes from memory
+  // about once per unit.  Softmax over a set does not depend on the order of
+  // its members.  Without a.rotate (keys and values that fit the last-level
+  // cache) the band is visited from tb up, which spreads the concurrent reads
+  // of a unit over many tiles.
+  const int qt_top = min(a.n_qtiles - 1, (a.n_chunks - 1 - cd) * a.qchunk + a.qchunk - 1);
+  const int tr = a.rotate ? min(max(tb, max(ta, max(0, band_start(qt_top * BM)) / BN)), tl + 1) : tb;
+  const int n_upper = tl - tr + 1;                    // band tiles tr .. tl
+  auto tile_j0 = [&](int it) {
+    if (it < ta) return it * BN;
+    const int k = it - ta;
+    return (k < n_upper ? tr + k : tb + (k - n_upper)) * BN;
+  };
   // Tile loads go through a buffer resource that spans exactly the tile's real
   // key rows (at most BN), so no address outside the inputs is ever touched;
   // rows past the last key re-read key n-1 (always masked by causality).
