@@ -28,9 +28,12 @@
 // fp32) the row is spread over 16-byte lanes and reduced with DPP.  For bf16
 // groups (G >= 2) the same work is a small dense contraction and runs on the
 // matrix cores (CDNA4 16x16x32 bf16 MFMA, G padded to 16 columns):
-//   S^T = K Q^T    A = 16 keys x 32 dims loaded straight from the cache into
-//                  the operand layout, B = Q^T kept in registers; lane l then
-//                  holds keys 4*(l/16) .. +3 of query head l % 16.
+//   S^T = K Q^T    A = 16 keys x 32 dims, B = Q^T kept in registers; lane l
+//                  then holds keys 4*(l/16) .. +3 of query head l % 16.  The K
+//                  tile is read from the cache in whole rows (4 rows of 256
+//                  bytes per load at head_dim 128; operand-layout loads, 16
+//                  rows x 64 bytes each, stream about 13 % slower) and passes
+//                  through the wave's LDS buffer, which then takes the V tile.
 //   O^T += V^T P^T B = P^T straight from the score registers (bf16), A = V^T
 //                  from a per-wave LDS copy of the V tile read with the
 //                  transposing LDS read; the key order inside each 32-key
@@ -73,12 +76,12 @@ int decode_scratch(void** out) {
 namespace {
 
 constexpr int kWaves = 4;          // waves per worker (work-group)
-// Keys per wave tile in the matrix-core loop: 32 keys (32 KB of LDS and
-// about 150 VGPRs per work-group, 3 work-groups per compute unit) for G <= 4;
-// 64 keys (2 per unit) for G = 8, whose larger partials make the extra
-// workers of the higher occupancy cost more in the merge than they gain.
+// Keys per wave tile in the matrix-core loop: 32 (8 KB of LDS per wave, about
+// 160 VGPRs at group 4 and 226 at group 8).  At group 8 the earlier 64-key
+// tiles (2 work-groups per compute unit) measured 2.8 % slower than 32-key
+// tiles once K no longer came in operand layout from HBM.
 template <int G>
-constexpr int mma_keys() { return G >= 8 ? 64 : 32; }
+constexpr int mma_keys() { return 32; }
 constexpr int kFastParts = 16;     // caches split over at most this many workers merge in one pass
 
 __device__ __forceinline__ int64_t worker_start(const DecodeArgs& a, int w) {
@@ -367,6 +370,7 @@ __global__ void __launch_bounds__(kWaves * 64, mma_keys<G>() == 32 ? 3 : 2) deco
   // Transposing V reads (tile independent): lane 16*q4 + 4e + a reads row
   // 4*q4 + e (+ 16 for the upper half of a 32-key step, + 32 per step),
   // columns 16*dt + 4a .. +3.
+  auto swk = [](int r) { return D == 128 ? (r & 15) : ((r >> 1) & 7); };
   int rd_off[DT];
   {
     const int vr = 4 * q4 + ((lane >> 2) & 3);
@@ -406,20 +410,37 @@ __global__ void __launch_bounds__(kWaves * 64, mma_keys<G>() == 32 ? 3 : 2) deco
       // their scores are masked to -inf below, so their weights, and with
       // them the re-read V rows, contribute exactly 0.
       const int last = hi - 1;
-      bf16x8 kop[NST][KS];
+      // K and V tiles in whole rows, 16-byte chunks: chunk u*64 + lane is
+      // row m / CPR, chunk m % CPR (4 whole 256-byte rows per load at D = 128).
+      bf16x8 kr[VLD], vr[VLD];
 #pragma unroll
-      for (int st = 0; st < NST; ++st) {
-        const bf16* kr = kb + int64_t(min(t0 + 16 * st + n, last)) * D + 8 * q4;
-#pragma unroll
-        for (int kk = 0; kk < KS; ++kk) kop[st][kk] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(kr + 32 * kk));
+      for (int u = 0; u < VLD; ++u) {
+        const int m = u * 64 + lane;
+        const int key = min(t0 + m / CPR, last);
+        kr[u] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(kb + int64_t(key) * D + (m % CPR) * 8));
       }
-      // V tile, row-major 16-byte chunks: chunk u*64 + lane is row / CPR, chunk % CPR.
-      bf16x8 vr[VLD];
 #pragma unroll
       for (int u = 0; u < VLD; ++u) {
         const int m = u * 64 + lane;
         const int key = min(t0 + m / CPR, last);
         vr[u] = __builtin_nontemporal_load(reinterpret_cast<const bf16x8*>(vb + int64_t(key) * D + (m % CPR) * 8));
+      }
+      // K passes through this wave's LDS buffer into the A-operand layout:
+      // chunk c of row r sits at chunk position c ^ swk(r), so the 16 rows read
+      // by a 16-lane group in one operand load hit distinct banks.
+#pragma unroll
+      for (int u = 0; u < VLD; ++u) {
+        const int m = u * 64 + lane;
+        const int r = m / CPR, c = m % CPR;
+        *reinterpret_cast<bf16x8*>(vs + r * RB + ((c ^ swk(r)) << 4)) = kr[u];
+      }
+      bf16x8 kop[NST][KS];
+#pragma unroll
+      for (int st = 0; st < NST; ++st) {
+        const int r = 16 * st + n;
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk)
+          kop[st][kk] = *reinterpret_cast<const bf16x8*>(vs + r * RB + (((4 * kk + q4) ^ swk(r)) << 4));
       }
 
       f32x4 s[NST];
