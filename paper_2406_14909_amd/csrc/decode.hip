@@ -82,7 +82,7 @@ constexpr int kWaves = 4;          // waves per worker (work-group)
 // tiles once K no longer came in operand layout from HBM.
 template <int G>
 constexpr int mma_keys() { return 32; }
-constexpr int kFastParts = 16;     // caches split over at most this many workers merge in one pass
+constexpr int kFastParts = 32;     // caches split over at most this many workers merge in one pass
 
 __device__ __forceinline__ int64_t worker_start(const DecodeArgs& a, int w) {
   return int64_t(w) * a.per_worker + (int64_t(w) * a.rem) / a.workers;
@@ -528,7 +528,7 @@ __global__ void __launch_bounds__(kWaves * 64, mma_keys<G>() == 32 ? 3 : 2) deco
 // o = sum_p 2^(m_p - M) acc_p / sum_p 2^(m_p - M) l_p, M = max_p m_p.
 // One work-group per (sequence, KV head, slice of at most 2 query heads): a
 // whole group of 8 heads per work-group left a GQA merge to only B * H_kv
-// work-groups, each reading up to 16 partials of every head.  The partials of
+// work-groups, each reading all the partials of every head.  The partials of
 // workers w0..w1 sit at consecutive slots w0 + cache .. w1 + cache.  Thread
 // groups of TPR threads (one float4 of each of the slice's head rows) take
 // every PG-th partial, so PG partial rows are read at once; the groups' sums

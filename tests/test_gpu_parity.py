@@ -268,7 +268,7 @@ DECODE_CASES = [
     ("bf16", 1, 64, 8, 128, 64, [5000, 1, 3000, 64, 700, 4999, 128, 2048], 5100, 2),  # G = 8
     ("bf16", 4, 16, 2, 64, 3, [1, 2], 5, 4),                  # G = 8, one worker for the batch
     ("bf16", 8, 8, 8, 128, 64, [3000, 17, 900, 2999, 1, 1500, 333, 2000], 3000, 2),  # many workers
-    ("bf16", 1, 16, 4, 64, 16, [30000, 5, 70000, 1], 70000, 2),  # G = 4, one cache over > 16 workers
+    ("bf16", 1, 16, 4, 64, 16, [30000, 5, 70000, 1], 70000, 2),  # G = 4, one cache over > 32 workers
     # every other (dtype, head_dim, group) instantiation the plan accepts
     ("bf16", 3, 4, 4, 64, 8, [10, 700, 1300, 64], 1400, 3),   # bf16 G = 1, head_dim 64
     ("f32", 2, 4, 4, 128, 16, [1, 500, 1200, 77], 1300, 3),   # fp32 G = 1, head_dim 128
