@@ -82,7 +82,10 @@ constexpr int kWaves = 4;          // waves per worker (work-group)
 // tiles once K no longer came in operand layout from HBM.
 template <int G>
 constexpr int mma_keys() { return 32; }
-constexpr int kFastParts = 32;     // caches split over at most this many workers merge in one pass
+// Caches split over at most fast_parts<G>() workers merge in one pass: 32 for
+// GQA groups (their caches span up to about 24 workers), 16 otherwise.
+template <int G>
+constexpr int fast_parts() { return G >= 4 ? 32 : 16; }
 
 __device__ __forceinline__ int64_t worker_start(const DecodeArgs& a, int w) {
   return int64_t(w) * a.per_worker + (int64_t(w) * a.rem) / a.workers;
@@ -561,6 +564,7 @@ __global__ void __launch_bounds__(256) decode_combine_kernel(DecodeArgs a) {
   const float* part0 = a.part + (int64_t(w0) + bg) * G * PS;
   auto at = [&](int p, int h) { return part0 + (int64_t(p) * G + h0 + h) * PS; };
 
+  constexpr int kFastParts = fast_parts<G>();
   if (np <= kFastParts) {
     // Few partials (the common case): every thread of the first TPR loads
     // (m, l, its float4 of acc) of all of them at once and merges in one pass.
