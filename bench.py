@@ -209,6 +209,10 @@ def main() -> int:
     ap.add_argument("--influence-items", type=int, default=4, help="calibration items for --influence")
     ap.add_argument("--rule-loss", action="store_true",
                     help="time the rule-loss table (moa_rule_loss): 54 rules x 1024 heads at --influence-n")
+    ap.add_argument("--power", choices=["prefill", "decode", "mfma"], default=None,
+                    help="run one kernel of the workload (or the MFMA-only calibration loop) for --power-seconds "
+                         "while sampling the board's socket power and shader clock with amd-smi")
+    ap.add_argument("--power-seconds", type=float, default=12.0)
     ap.add_argument("--peaks", action="store_true",
                     help="measure practical ceilings: hipBLASLt bf16 GEMM TFLOP/s and streaming-read GB/s")
     args = ap.parse_args()
@@ -223,6 +227,9 @@ def main() -> int:
 
     if args.peaks:
         print(json.dumps(measure_peaks()), flush=True)
+        return 0
+    if args.power:
+        print(json.dumps(measure_power(args)), flush=True)
         return 0
     if args.influence:
         print(json.dumps(measure_influence(args)), flush=True)
@@ -525,6 +532,105 @@ def measure_configs(M, workloads, reps: int):
         torch.cuda.empty_cache()
         out[name] = entry
     return out
+
+
+def sample_power(stop, out, delay=4.0, period=0.5):
+    """Appends (socket W, mean shader MHz, min, max) from `amd-smi metric` every
+    `period` seconds, after `delay` seconds of warm-up, until stop is set."""
+    import subprocess
+
+    if stop.wait(delay):
+        return
+    while not stop.is_set():
+        try:
+            r = subprocess.run(["amd-smi", "metric", "--power", "--clock", "--json"], capture_output=True,
+                               text=True, timeout=10)
+            for g in json.loads(r.stdout).get("gpu_data", [])[:1]:
+                clks = [v["clk"]["value"] for k, v in g["clock"].items() if k.startswith("gfx_")]
+                out.append((float(g["power"]["socket_power"]["value"]), sum(clks) / len(clks), min(clks), max(clks)))
+        except Exception as e:                                    # no amd-smi, or a format it does not know
+            log(f"[bench] power sample failed: {e}")
+            return
+        stop.wait(period)
+
+
+def measure_power(args):
+    """Board power and shader clock while one kernel runs back to back.
+
+    The hot path is bound by the board's power limit when the matrix cores
+    and vector ALUs work together: the clock then drops below what a pure
+    matrix-core load keeps.  prefill / decode: the workload's moa_prefill /
+    moa_decode (one cache set) repeated for --power-seconds; mfma: the
+    MFMA-only calibration loop held for the same time.  Rate: in-band
+    TFLOP/s, HBM GB/s or the loop's TFLOP/s; energy per unit = power / rate."""
+    import threading
+
+    import torch
+
+    sys.path.insert(0, os.path.dirname(os.path.abspath(__file__)))
+    samples, stop = [], threading.Event()
+    sampler = threading.Thread(target=sample_power, args=(stop, samples), daemon=True)
+    res = {"kernel": args.power, "workload": args.workload}
+    if args.power == "mfma":
+        import subprocess
+
+        probe = os.path.join(ROOT, "paper_2406_14909_amd", "_build", "mfma_loop")
+        sampler.start()
+        out = subprocess.run([probe, str(args.power_seconds)], capture_output=True, text=True, timeout=300).stdout
+        stop.set()
+        rate = float([l.split()[1] for l in out.splitlines() if l.startswith("hold ")][0])
+        res.update({"rate": rate, "unit": "TFLOP/s"})
+    else:
+        import workloads
+        from paper_2406_14909_amd import moa as M
+
+        wl = workloads.workload(args.workload)
+        B, N = wl.decode_batch, wl.n
+        plan = M.moa_plan(wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.num_sink, N, wl.dtype, wl.alpha, wl.beta)
+        dt = wl.torch_dtype()
+        if args.power == "prefill":
+            q = workloads.randn((B, N, wl.num_q_heads, wl.head_dim), 1, dt, "cuda")
+            k = workloads.randn((B, N, wl.num_kv_heads, wl.head_dim), 2, dt, "cuda")
+            v = workloads.randn((B, N, wl.num_kv_heads, wl.head_dim), 3, dt, "cuda")
+            o = torch.empty_like(q)
+            call = lambda: M.moa_prefill(plan, q, k, v, o)
+            group = wl.num_q_heads // wl.num_kv_heads
+            work = 4.0 * wl.head_dim * B * group * sum(visible_pairs(N, int(w), wl.num_sink) for w in plan.window) / 1e12
+            unit = "TFLOP/s"
+        else:
+            k = workloads.randn((B, N + 1, wl.num_kv_heads, wl.head_dim), 5, dt, "cuda")
+            v = workloads.randn((B, N + 1, wl.num_kv_heads, wl.head_dim), 6, dt, "cuda")
+            q = workloads.randn((B, wl.num_q_heads, wl.head_dim), 7, dt, "cuda")
+            kc, vc, pos = M.new_cache(plan, B)
+            M.moa_kv_append(plan, kc, vc, pos, k, v, 0)
+            del k, v
+            ws = M.new_workspace(plan, B)
+            o = torch.empty_like(q)
+            call = lambda: M.moa_decode(plan, q, kc, vc, N, ws, o)
+            esz = 2 if wl.dtype == "bf16" else 4
+            work = B * sum(min(N + 1, int(c)) for c in plan.capacity) * wl.head_dim * 2 * esz / 1e9
+            unit = "GB/s"
+        call()
+        torch.cuda.synchronize()
+        sampler.start()
+        t0, calls = time.perf_counter(), 0
+        while time.perf_counter() - t0 < args.power_seconds:
+            for _ in range(10):
+                call()
+            torch.cuda.synchronize()
+            calls += 10
+        elapsed = time.perf_counter() - t0
+        stop.set()
+        res.update({"rate": round(work * calls / elapsed, 1), "unit": unit, "calls": calls})
+    sampler.join(timeout=15)
+    if samples:
+        pw = sum(s[0] for s in samples) / len(samples)
+        res.update({"socket_power_w": round(pw, 1), "shader_clock_mhz": round(sum(s[1] for s in samples) / len(samples)),
+                    "shader_clock_min_mhz": min(s[2] for s in samples), "shader_clock_max_mhz": max(s[3] for s in samples),
+                    "samples": len(samples),
+                    "energy_per_unit": round(pw / res["rate"], 4),
+                    "energy_unit": "pJ/FLOP" if res["unit"] == "TFLOP/s" else "J/GB"})
+    return res
 
 
 def measure_influence(args):

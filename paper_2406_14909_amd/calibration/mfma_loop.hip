@@ -5,10 +5,13 @@
 // the practical roof for MFMA-bound kernels on this GPU (the published
 // 2.5 PFLOP/s assumes the peak clock, which the part does not hold under a
 // full matrix load).  Prints one line per configuration and a final
-// "best <TFLOP/s>" line.
+// "best <TFLOP/s>" line.  With an argument S > 0 it then keeps the 2-waves-
+// per-SIMD configuration running for about S seconds (for sampling the board
+// power and clock under a pure matrix load) and prints "hold <TFLOP/s>".
 #include <hip/hip_runtime.h>
 
 #include <cstdio>
+#include <cstdlib>
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -37,7 +40,8 @@ __global__ void __launch_bounds__(256) mfma_loop(float* out, float seed, int ite
   out[blockIdx.x * blockDim.x + threadIdx.x] = s;   // keeps the products
 }
 
-int main() {
+int main(int argc, char** argv) {
+  const double hold_s = argc > 1 ? std::atof(argv[1]) : 0.0;
   const int max_blocks = 4096;
   float* out = nullptr;
   if (hipMalloc(&out, sizeof(float) * max_blocks * 256) != hipSuccess) {
@@ -72,6 +76,25 @@ int main() {
     best = tf > best ? tf : best;
   }
   std::printf("best %.1f\n", best);
+  if (hold_s > 0.0) {
+    const int blocks = cus * 2, iters = kStepsPerSimd / 2;
+    hipEvent_t e0, e1;
+    if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) return 1;
+    double flops = 0.0, ms_total = 0.0;
+    while (ms_total < hold_s * 1e3) {
+      (void)hipEventRecord(e0);
+      hipLaunchKernelGGL(mfma_loop, dim3(blocks), dim3(256), 0, 0, out, 1e-3f, iters);
+      (void)hipEventRecord(e1);
+      if (hipEventSynchronize(e1) != hipSuccess) return 1;
+      float ms = 0.0f;
+      (void)hipEventElapsedTime(&ms, e0, e1);
+      ms_total += ms;
+      flops += double(blocks) * 4 * iters * 4 * 2.0 * 32 * 32 * 16;
+    }
+    (void)hipEventDestroy(e0);
+    (void)hipEventDestroy(e1);
+    std::printf("hold %.1f\n", flops / (ms_total / 1e3) / 1e12);
+  }
   (void)hipFree(out);
   return 0;
 }
