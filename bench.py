@@ -209,7 +209,7 @@ def main() -> int:
     ap.add_argument("--influence-items", type=int, default=4, help="calibration items for --influence")
     ap.add_argument("--rule-loss", action="store_true",
                     help="time the rule-loss table (moa_rule_loss): 54 rules x 1024 heads at --influence-n")
-    ap.add_argument("--power", choices=["prefill", "decode", "mfma"], default=None,
+    ap.add_argument("--power", choices=["prefill", "decode", "influence", "mfma"], default=None,
                     help="run one kernel of the workload (or the MFMA-only calibration loop) for --power-seconds "
                          "while sampling the board's socket power and shader clock with amd-smi")
     ap.add_argument("--power-seconds", type=float, default=12.0)
@@ -588,7 +588,17 @@ def measure_power(args):
         B, N = wl.decode_batch, wl.n
         plan = M.moa_plan(wl.num_q_heads, wl.num_kv_heads, wl.head_dim, wl.num_sink, N, wl.dtype, wl.alpha, wl.beta)
         dt = wl.torch_dtype()
-        if args.power == "prefill":
+        if args.power == "influence":
+            n, items = args.influence_n, args.influence_items
+            q = workloads.randn((items, n, wl.num_q_heads, wl.head_dim), 11, torch.bfloat16, "cuda")
+            k = workloads.randn((items, n, wl.num_kv_heads, wl.head_dim), 12, torch.bfloat16, "cuda")
+            v = workloads.randn((items, n, wl.num_kv_heads, wl.head_dim), 13, torch.bfloat16, "cuda")
+            do = workloads.randn((items, n, wl.num_q_heads, wl.head_dim), 14, torch.bfloat16, "cuda")
+            ebar = M.moa_influence(q, k, v, do)
+            call = lambda: M.moa_influence(q, k, v, do, ebar)
+            work = 8.0 * wl.head_dim * (n * (n + 1) // 2) * wl.num_q_heads * items / 1e12
+            unit = "TFLOP/s"
+        elif args.power == "prefill":
             q = workloads.randn((B, N, wl.num_q_heads, wl.head_dim), 1, dt, "cuda")
             k = workloads.randn((B, N, wl.num_kv_heads, wl.head_dim), 2, dt, "cuda")
             v = workloads.randn((B, N, wl.num_kv_heads, wl.head_dim), 3, dt, "cuda")
