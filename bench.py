@@ -527,6 +527,7 @@ def measure_configs(M, workloads, reps: int):
                                "peak": HBM_PEAK_GBS, "frac": round(gbs / HBM_PEAK_GBS, 4),
                                "tokens_per_s": round(B / (ms / 1e3), 1),
                                "bytes_per_call": round(float(np.mean(nbytes))), "cache_sets": sets_n,
+                               "traffic": measured_traffic(f"hbm_traffic__decode_kernel__{name}.md"),
                                "kernel": f"moa_decode ({kern} + decode_combine_kernel)", "calls_timed": reps}
             del sets, kn, vn, qn, ws, o
         torch.cuda.empty_cache()
