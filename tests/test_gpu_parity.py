@@ -286,6 +286,39 @@ def test_decode_matches_oracle(case):
     _decode_run(*case, seed=50, poison=True)
 
 
+SINGLE_KEY_CASES = [
+    # dtype, B, Hq, Hkv, D (one case per decode kernel family and group size)
+    ("bf16", 3, 4, 4, 128),     # vector-ALU kernel, G = 1
+    ("bf16", 3, 8, 4, 128),     # matrix-core kernel, G = 2
+    ("bf16", 2, 16, 4, 64),     # matrix-core kernel, G = 4, head_dim 64
+    ("bf16", 64, 64, 8, 128),   # matrix-core kernel, G = 8, 512 slots: two workers
+    ("f32", 2, 4, 4, 64),       # fp32, G = 1
+    ("f32", 2, 64, 8, 128),     # fp32, G = 8
+]
+
+
+@pytest.mark.parametrize("case", SINGLE_KEY_CASES, ids=lambda c: f"{c[0]}-B{c[1]}-hq{c[2]}-hkv{c[3]}-d{c[4]}")
+def test_decode_of_a_single_cached_key_returns_its_value(case):
+    """Decode at position 0: every cache holds one key, whose softmax weight is
+    exactly 1 (paper Sec. 2.1, Eq. 1 over a one-element set), so each output
+    row is the cached value of its KV head, bit for bit in either dtype."""
+    dt, bsz, hq, hkv, d = case
+    _say("decode single key", case)
+    dtype = DT[dt]
+    plan, _ = _plan(hq, hkv, d, 4, 64, dt, [1 + 9 * g for g in range(hkv)])
+    q, k, v = _inputs(bsz, 1, hq, hkv, d, dtype, 70)
+    kc, vc, pos = M.new_cache(plan, bsz)
+    ws = M.new_workspace(plan, bsz)
+    ws.fill_(0xFF)
+    M.moa_kv_append(plan, kc, vc, pos, k, v, 0)
+    o, buf = guarded_empty((bsz, hq, d), dtype)
+    M.moa_decode(plan, q[:, 0].contiguous(), kc, vc, 0, ws, o)
+    torch.cuda.synchronize()
+    assert guard_intact(buf, (bsz, hq, d))
+    want = v[:, 0].repeat_interleave(hq // hkv, dim=1)      # q head h reads KV head h // G
+    assert torch.equal(bits(o), bits(want))
+
+
 def test_decode_equals_prefill_row():
     _say("decode vs prefill row")
     bsz, hq, hkv, d, s, n = 2, 8, 2, 128, 8, 900
