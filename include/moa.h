@@ -187,9 +187,9 @@ size_t moa_decode_workspace_bytes(const moa_plan_t* plan, int32_t batch);
  * need no initialisation and are meaningless after the call.  Calls that
  * share one workspace must be ordered on one stream.  Neither o nor the
  * workspace may overlap q, the caches or each other (MOA_ERR_INVALID_ARG).
- * Launches one kernel, or
- * two when some head's cache spans several split-K chunks (the second merges
- * the chunks' partial results). */
+ * Launches one kernel when the whole call fits one work-group, otherwise two
+ * (the second merges the partial results of caches split between
+ * work-groups). */
 moa_status_t moa_decode(const moa_plan_t* plan, const void* q, const void* k_cache,
                         const void* v_cache, void* o, int32_t batch, int64_t pos,
                         void* workspace, size_t ws_bytes, void* hip_stream);
